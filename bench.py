@@ -1,0 +1,162 @@
+#!/usr/bin/env python3
+"""Benchmark of the surrogate-inference region on one MI355X.
+
+One step = one pass of the whole hot path over the workload: the fused
+gather -> MLP -> scatter (``hpacml_infer``) plus the collect records of the
+region's inputs and outputs (``hpacml_collect`` twice into one [B x (F_in +
+F_out)] buffer).  Inputs are synthetic, seeded and resident in HBM before the
+timed region.  Prints one JSON line.
+
+Default workload: bond-pricing surrogate, 1,048,576 points, 9 SoA fp32 inputs,
+MLP 9 -> 128 -> 128 -> 128 -> 1 (ReLU), fp32.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {"f32": 157.3e12, "bf16": 2.5e15}   # dense MFMA peaks of MI355X, flop/s
+HBM_PEAK = 8.0e12                          # bytes/s
+
+DESCRIPTION = {
+    "options": "option pricing: 65,536 points, 5 SoA fp32 inputs, MLP 5-64-64-1 ReLU fp32, 1 output",
+    "bonds": "bond pricing: 1,048,576 points, 9 SoA fp32 inputs U[0,1], MLP 9-128-128-128-1 ReLU fp32, "
+             "1 output; collect records 9+1 values per point",
+    "stencil2d": "2-D stencil: 2048x2048 grid x 4 fp32 fields, periodic 3x3 window (36 features), "
+                 "MLP 36-128-128-4 ReLU fp32, 4 outputs per cell",
+    "poses": "pose scoring: 4,194,304 poses, 6 fp32 inputs, MLP 6-256-256-256-1 ReLU, bf16 weights and "
+             "activations with fp32 accumulate, 1 output",
+    "stencil3d": "3-D stencil: 512^3 grid x 5 fp32 fields, periodic 7-point window (35 features), "
+                 "MLP 35-512-512-5 ReLU, bf16 with fp32 accumulate, 5 outputs per cell",
+}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="bonds", choices=sorted(DESCRIPTION))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU work for the oracle sample")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(see the sharding notes in the design document)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2407_18352_amd import _abi, api
+    from paper_2407_18352_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    t0 = time.time()
+    w = wl.make(args.workload)
+    print("[bench] workload %s generated in %.1fs" % (args.workload, time.time() - t0), file=sys.stderr, flush=True)
+
+    ins = [torch.from_numpy(a).cuda() for a in w.inputs]
+    outs = [torch.from_numpy(a).cuda() for a in w.outputs]
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.FROM)
+    mo_rec = api.Map(w.out_spec, outs, _abi.TO)        # the outputs as a recorded map
+    model = api.Model(w.model)
+    variant = api.variant(model, mi, mo)
+    B, Fi, Fo = mi.n_points, mi.n_features, mo.n_features
+    ld = Fi + Fo
+    rec = torch.empty((B, ld), device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        api.infer(model, mi, mo, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        api.collect(mi, rec, ld, stream)
+        api.collect(mo_rec, rec[:, Fi:], ld, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = start.elapsed_time(stop)
+    infer_ms = [a.elapsed_time(b) for a, b in evs]
+    ms_step = total_ms / args.steps
+    infer_avg = float(np.mean(infer_ms))
+
+    flops_pt = w.flops_per_point
+    achieved = flops_pt * B / (infer_avg * 1e-3)
+    peak = PEAK[w.compute]
+    result = {
+        "metric": "surrogate points/sec (gather+MLP+scatter) and % of HBM / MFMA roofline",
+        "value": B / (ms_step * 1e-3),
+        "unit": "points/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.compute,
+        "data": "synthetic (seeded generators; random-init He-normal weights)",
+        "config": {"workload": DESCRIPTION[args.workload], "points": B, "features_in": Fi,
+                   "features_out": Fo, "dims": w.dims, "kernel": variant},
+        "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": variant, "kernel_avg_ms": infer_avg,
+                     "algorithmic_flop_per_launch": flops_pt * B},
+        "infer_points_per_s": B / (infer_avg * 1e-3),
+        "infer_ms": {"mean": infer_avg, "median": float(np.median(infer_ms)), "min": float(np.min(infer_ms))},
+        "collect_ms_per_step": ms_step - infer_avg,
+        "wall_s_timed": wall,
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        # bounded sample: as many leading rows as fit the CPU-time target,
+        # estimated from a short calibration run
+        n_cal = min(B, 4096)
+        rows = np.arange(n_cal, dtype=np.int64)
+        c0 = time.perf_counter()
+        oracle.infer_rows(w.in_spec, w.inputs, w.model, rows)
+        per_pt = (time.perf_counter() - c0) / n_cal
+        n = int(min(B, max(n_cal, args.cpu_seconds / max(per_pt, 1e-12))))
+        rows = wl.sample_rows(B, n, seed_k=998)
+        c0 = time.perf_counter()
+        Y = oracle.infer_rows(w.in_spec, w.inputs, w.model, rows)
+        cpu_s = time.perf_counter() - c0
+        got = np.stack([o.cpu().numpy().reshape(-1)[rows] for o in outs], 1).astype(np.float64)
+        s = np.sqrt(np.mean(Y.astype(np.float64) ** 2, axis=0, keepdims=True))
+        worst = float(np.max(np.abs(got - Y) / np.maximum(np.abs(Y), s)))
+        result["cpu_baseline"] = {"value": len(rows) / cpu_s, "unit": "points/s", "cores": oracle.num_threads(),
+                                  "kind": "oracle",
+                                  "sample": "%d of %d sweep rows (seeded), gather+MLP in fp64, %.1fs"
+                                            % (len(rows), B, cpu_s)}
+        result["parity_on_cpu_sample"] = {"worst_scaled_error": worst, "rtol": 1e-5 if w.compute == "f32" else 2e-2}
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,205 @@
+/*
+ * hpacml.h -- C ABI of an MI355X (gfx950) library for HPAC-ML's
+ * surrogate-inference region (arXiv 2407.18352).
+ *
+ * A region replaces an annotated scientific kernel by a neural-network
+ * surrogate.  Its inputs are described by a tensor functor (a per-point access
+ * pattern with symbolic indices, Sec. III-B, Fig. 2) applied by a tensor map to
+ * concrete application arrays over a concrete index sweep (Sec. III-C, Fig. 3);
+ * the map turns the arrays into a dense [points x features] tensor
+ * (Sec. IV-A: extraction, resolution, wrapping, composition).  The model runs
+ * on that tensor and a `from` map writes its outputs back into application
+ * arrays (Sec. IV-A, last paragraph; Sec. IV-B).  Collect mode records the
+ * mapped values instead of running the model (Sec. III-A-2, Sec. IV-B).
+ *
+ * Every pointer to application data is a DEVICE pointer on the current HIP
+ * device.  The stream argument is a hipStream_t passed as void* (NULL = the
+ * null stream).  No function throws; every failure is reported as a status,
+ * and every check is done on the host before anything is enqueued, so a call
+ * that fails writes nothing.  `*out` handles are set to NULL on failure.
+ *
+ * Thread safety: handles are immutable after creation.  Concurrent infer and
+ * collect calls with the same handles on different streams are allowed.
+ */
+#ifndef HPACML_H
+#define HPACML_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HPACML_ABI_VERSION 1
+#define HPACML_MAX_RANK 4         /* spatial dimensions of a functor / sweep */
+#define HPACML_MAX_SLICES 64      /* right-hand-side slices per functor */
+#define HPACML_MAX_TARGETS 64     /* arrays per map */
+#define HPACML_MAX_FEATURES 256   /* features per point of one map */
+#define HPACML_MAX_LAYERS 8       /* layers per model */
+#define HPACML_MAX_WIDTH 1024     /* width of any layer */
+
+typedef enum {
+    HPACML_OK = 0,
+    HPACML_E_INVAL = 1,       /* NULL or malformed argument, non-device pointer */
+    HPACML_E_SHAPE = 2,       /* feature / point counts do not agree */
+    HPACML_E_RANGE = 3,       /* an access leaves an array without a boundary mode */
+    HPACML_E_ALIAS = 4,       /* a `from` target overlaps a `to` target unsafely */
+    HPACML_E_UNSUPPORTED = 5, /* valid request outside this library's limits */
+    HPACML_E_NOMEM = 6,       /* device or host allocation failed */
+    HPACML_E_DEVICE = 7       /* HIP runtime error (launch, copy, no device) */
+} hpacml_status;
+
+/* direction of a tensor map (Sec. III-C, direction-specifier) */
+enum { HPACML_TO = 0, HPACML_FROM = 1 };
+/* per-dimension handling of accesses outside [0, extent); the paper maps only
+ * interiors, so NONE makes such an access an error (HPACML_E_RANGE) */
+enum { HPACML_BND_NONE = 0, HPACML_BND_PERIODIC = 1, HPACML_BND_CLAMP = 2 };
+/* element / compute types */
+enum { HPACML_F32 = 0, HPACML_BF16 = 1 };
+/* per-layer activation */
+enum { HPACML_ACT_IDENTITY = 0, HPACML_ACT_RELU = 1 };
+
+/* One right-hand-side slice of a tensor functor (Sec. III-B; Sec. IV-A,
+ * Symbolic Shape Extraction).  In dimension d the slice covers the symbol's
+ * value s_d plus lo[d], lo[d]+1, ..., lo[d]+count[d]-1.  Example: the slice
+ * [i, j-1:j+2] is lo = {0, -1}, count = {1, 3}.  Entries at d >= rank are
+ * ignored.  count[d] >= 1. */
+typedef struct {
+    int32_t lo[HPACML_MAX_RANK];
+    int32_t count[HPACML_MAX_RANK];
+} hpacml_slice;
+
+/* A tensor functor [s_0, ..., s_{rank-1}, 0:n_features] = (slices...).
+ * Applied to T targets, each target contributes every slice's elements;
+ * features are ordered target-major, then slice order, then row-major over
+ * the slice's counts (Sec. IV-A, Tensor Composition: flatten, then
+ * concatenate).  n_features must equal T * sum over slices of prod(count). */
+typedef struct {
+    int32_t rank;                 /* 1..HPACML_MAX_RANK */
+    int32_t n_slices;             /* 1..HPACML_MAX_SLICES */
+    const hpacml_slice *slices;   /* [n_slices], read during the call only */
+    int32_t n_features;
+} hpacml_functor;
+
+/* An application array, borrowed: the library keeps the pointer, never a copy
+ * (Sec. IV-A, Tensor Wrapping).  extent and stride are in elements; element
+ * (x_0, ..., x_{rank-1}) is data[sum_d x_d * stride[d]].  Strides may be any
+ * non-negative values (views).  All targets of one map share extents. */
+typedef struct {
+    void *data;                   /* device pointer */
+    int32_t dtype;                /* HPACML_F32 only */
+    int32_t reserved;             /* must be 0 */
+    int64_t extent[HPACML_MAX_RANK];
+    int64_t stride[HPACML_MAX_RANK];
+} hpacml_array;
+
+/* The concrete slice of a map target, per dimension [start:stop:step], stop
+ * exclusive, step >= 1 (Sec. III-C, cs-specifier: [1:N] is 1..N-1).  The sweep
+ * has prod_d ceil((stop-start)/step) points, numbered row-major (last dimension
+ * fastest); that number is the point's row in the composed tensor.
+ * 0 <= start <= stop <= extent. */
+typedef struct {
+    int64_t start[HPACML_MAX_RANK];
+    int64_t stop[HPACML_MAX_RANK];
+    int64_t step[HPACML_MAX_RANK];
+} hpacml_sweep;
+
+typedef struct hpacml_map_s hpacml_map;
+typedef struct hpacml_model_s hpacml_model;
+
+/* Checks a map description without touching any device: functor shape,
+ * feature count, sweep bounds, boundary modes and every access of every sweep
+ * point against the extents.  On success writes the number of points and
+ * features (either output pointer may be NULL).  Returns the status
+ * hpacml_map_create would return for the same arguments, except for checks of
+ * the data pointers themselves (device residency).
+ *   f, targets, sweep, bnd: read during the call only.
+ *   dir: HPACML_TO or HPACML_FROM.  A FROM map must use one slice with one
+ *        element per dimension (each point writes one element per target);
+ *        otherwise HPACML_E_UNSUPPORTED.  CLAMP with a nonzero offset on a FROM
+ *        map is HPACML_E_INVAL (two points would write one element).
+ *   bnd: [rank] boundary modes. */
+hpacml_status hpacml_map_validate(const hpacml_functor *f, int32_t dir,
+                                  const hpacml_array *targets, int32_t n_targets,
+                                  const hpacml_sweep *sweep, const int32_t *bnd,
+                                  int64_t *n_points, int32_t *n_features);
+
+/* Creates a tensor map (Sec. III-C, `tensor map(to|from: functor(targets))`):
+ * validates as hpacml_map_validate, checks that every target pointer is device
+ * memory (HPACML_E_INVAL otherwise), builds the access plan (Sec. IV-A
+ * extraction + resolution + wrapping, done once per map) and uploads it.  May
+ * synchronise the device.  The caller keeps the arrays alive while work that
+ * uses the map is in flight. */
+hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir,
+                                const hpacml_array *targets, int32_t n_targets,
+                                const hpacml_sweep *sweep, const int32_t *bnd,
+                                hpacml_map **out);
+
+/* Points (rows) and features (columns) of the map's tensor. */
+hpacml_status hpacml_map_shape(const hpacml_map *m, int64_t *n_points, int32_t *n_features);
+
+/* Frees a map.  NULL-safe.  Synchronise streams that use it first. */
+void hpacml_map_destroy(hpacml_map *m);
+
+/* Checks a model description without touching any device (same status as
+ * hpacml_model_create would return for these arguments). */
+hpacml_status hpacml_model_validate(int32_t n_layers, const int32_t *dims,
+                                    const int32_t *act, int32_t compute);
+
+/* Creates a multilayer perceptron (the surrogate; the paper's models are
+ * TorchScript Linear/ReLU stacks, Sec. IV-B).  Layer l maps dims[l] inputs to
+ * dims[l+1] outputs: y = act[l](W[l] x + b[l]).
+ *   n_layers: 1..HPACML_MAX_LAYERS; dims: [n_layers+1], each 1..HPACML_MAX_WIDTH,
+ *             dims[0] <= HPACML_MAX_FEATURES.
+ *   W[l]: HOST fp32 [dims[l+1]][dims[l]] row-major (PyTorch Linear layout).
+ *   b[l]: HOST fp32 [dims[l+1]].
+ *   act:  [n_layers] HPACML_ACT_*.
+ *   compute: HPACML_F32 (fp32 everywhere) or HPACML_BF16 (weights, gathered
+ *            inputs and hidden activations rounded to bf16, nearest-even;
+ *            fp32 accumulation; fp32 biases and outputs).
+ * The weights are copied (and converted) into library-owned device memory;
+ * the caller may free its host arrays on return.  Synchronises the device. */
+hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims,
+                                  const float *const *W, const float *const *b,
+                                  const int32_t *act, int32_t compute,
+                                  hpacml_model **out);
+
+/* Frees a model.  NULL-safe.  Synchronise streams that use it first. */
+void hpacml_model_destroy(hpacml_model *m);
+
+/* Inference mode of a region (Sec. III-C `ml(infer)`, Sec. IV-B): for every
+ * sweep point, gather through `in` (a TO map), run the model, write the outputs
+ * through `out` (a FROM map).  Every point's inputs are read before its
+ * outputs are written, and a `from` target may overlap a `to` target only when
+ * both maps address exactly the same element per point (same array, zero
+ * offsets, same sweep); otherwise HPACML_E_ALIAS.  Requires
+ * points(in) == points(out), features(in) == dims[0] and
+ * features(out) == dims[n_layers] (HPACML_E_SHAPE).  Asynchronous on `stream`;
+ * returns HPACML_E_DEVICE only for launch errors.  Zero points: HPACML_OK,
+ * nothing launched. */
+hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in,
+                           const hpacml_map *out, void *stream);
+
+/* Collect mode (Sec. III-A-2, Sec. IV-B): the values a map addresses, copied
+ * bit for bit into dst[p * ld + f] for point p and feature f (a TO map records
+ * a region's inputs; a FROM map, the outputs it addresses).  dst is a DEVICE
+ * float buffer of n_points * ld elements; ld >= n_features.  Columns f >=
+ * n_features are not written, so two calls with dst and dst + F_in record
+ * input/output pairs in one buffer.  Asynchronous on `stream`. */
+hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *stream);
+
+/* Name of the kernel hpacml_infer would launch for these handles (a static
+ * string), or NULL when the arguments are invalid. */
+const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in,
+                                 const hpacml_map *out);
+
+/* Static, human-readable text of a status. */
+const char *hpacml_status_string(hpacml_status s);
+
+/* HPACML_ABI_VERSION of the built library. */
+int32_t hpacml_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HPACML_H */

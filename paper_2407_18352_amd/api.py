@@ -1,0 +1,177 @@
+"""Python binding of the C ABI, with torch tensors as device memory.
+
+Argument marshalling only: descriptors are filled from plain-data specs and
+tensor metadata, and the calls go straight to ``libhpacml.so``.  Specs have the
+form ``{"rank", "slices": [(lo, count), ...], "sweep": (start, stop, step),
+"bnd": [...]}`` (one right-hand-side slice per entry, Sec. III-B; the sweep is
+the concrete slice of a tensor map, Sec. III-C).
+"""
+from __future__ import annotations
+
+import ctypes as C
+
+from . import _abi
+from ._abi import check, lib
+
+
+def _functor(spec, n_targets, n_features=None):
+    R = min(max(int(spec["rank"]), 0), _abi.MAX_RANK)
+    slices = spec["slices"]
+    arr = (_abi.Slice * max(1, len(slices)))()
+    per = 0
+    for s, (lo, cnt) in enumerate(slices):
+        e = 1
+        for d in range(_abi.MAX_RANK):
+            arr[s].lo[d] = int(lo[d]) if d < R else 0
+            arr[s].count[d] = int(cnt[d]) if d < R else 1
+            if d < R:
+                e *= int(cnt[d])
+        per += e
+    f = _abi.Functor()
+    f.rank, f.n_slices = int(spec["rank"]), len(slices)
+    f.slices = C.cast(arr, C.POINTER(_abi.Slice))
+    f.n_features = per * n_targets if n_features is None else int(n_features)
+    return f, arr
+
+
+def _sweep(spec):
+    R = min(max(int(spec["rank"]), 0), _abi.MAX_RANK)
+    sw = _abi.Sweep()
+    start, stop, step = spec["sweep"]
+    for d in range(_abi.MAX_RANK):
+        sw.start[d] = int(start[d]) if d < R else 0
+        sw.stop[d] = int(stop[d]) if d < R else 1
+        sw.step[d] = int(step[d]) if d < R else 1
+    bl = [int(b) for b in spec.get("bnd", [0] * R)][:R]
+    bnd = (C.c_int32 * _abi.MAX_RANK)(*(bl + [0] * (_abi.MAX_RANK - len(bl))))
+    return sw, bnd
+
+
+def array_desc(data_ptr: int, shape, strides, dtype: int = _abi.F32):
+    """An ``hpacml_array`` from raw metadata (strides in elements)."""
+    a = _abi.Array()
+    a.data = C.c_void_p(int(data_ptr))
+    a.dtype = dtype
+    a.reserved = 0
+    for d in range(_abi.MAX_RANK):
+        a.extent[d] = int(shape[d]) if d < len(shape) else 1
+        a.stride[d] = int(strides[d]) if d < len(strides) else 0
+    return a
+
+
+def _tensor_desc(t):
+    import torch
+    if t.dtype != torch.float32:
+        raise TypeError("map targets must be float32 tensors")
+    return array_desc(t.data_ptr(), tuple(t.shape), tuple(t.stride()))
+
+
+def validate_map(spec, arrays, direction: int, n_features=None):
+    """``hpacml_map_validate`` on descriptors (no device access).  ``arrays`` are
+    ``hpacml_array`` structures (see ``array_desc``).  Returns
+    ``(status, n_points, n_features)``."""
+    f, keep = _functor(spec, len(arrays), n_features)
+    sw, bnd = _sweep(spec)
+    tarr = (_abi.Array * max(1, len(arrays)))(*arrays)
+    npts, nfeat = C.c_int64(-1), C.c_int32(-1)
+    st = lib().hpacml_map_validate(C.byref(f), direction, tarr, len(arrays), C.byref(sw), bnd,
+                                   C.byref(npts), C.byref(nfeat))
+    return st, npts.value, nfeat.value
+
+
+def validate_model(dims, act, compute: int):
+    L = len(dims) - 1
+    d = (C.c_int32 * len(dims))(*dims)
+    a = (C.c_int32 * max(1, len(act)))(*act)
+    return lib().hpacml_model_validate(L, d, a, compute)
+
+
+class Map:
+    """A tensor map over torch tensors (device memory is borrowed: keep the
+    tensors alive while work that uses the map is in flight)."""
+
+    def __init__(self, spec, targets, direction: int, n_features=None):
+        self.targets = list(targets)
+        f, keep = _functor(spec, len(self.targets), n_features)
+        sw, bnd = _sweep(spec)
+        tarr = (_abi.Array * max(1, len(self.targets)))(*[_tensor_desc(t) for t in self.targets])
+        h = C.c_void_p()
+        check(lib().hpacml_map_create(C.byref(f), direction, tarr, len(self.targets), C.byref(sw), bnd,
+                                      C.byref(h)), "hpacml_map_create")
+        self.handle = h
+        npts, nfeat = C.c_int64(), C.c_int32()
+        check(lib().hpacml_map_shape(h, C.byref(npts), C.byref(nfeat)), "hpacml_map_shape")
+        self.n_points, self.n_features = npts.value, nfeat.value
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().hpacml_map_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Model:
+    """A surrogate MLP; weights are host fp32 arrays [out][in] (numpy or torch
+    CPU), copied into library-owned device memory."""
+
+    def __init__(self, spec):
+        import numpy as np
+        dims = [int(x) for x in spec["dims"]]
+        L = len(dims) - 1
+        self.W = [np.ascontiguousarray(np.asarray(w, dtype=np.float32)) for w in spec["W"]]
+        self.b = [np.ascontiguousarray(np.asarray(b, dtype=np.float32)) for b in spec["b"]]
+        Wp = (C.POINTER(C.c_float) * L)(*[w.ctypes.data_as(C.POINTER(C.c_float)) for w in self.W])
+        bp = (C.POINTER(C.c_float) * L)(*[b.ctypes.data_as(C.POINTER(C.c_float)) for b in self.b])
+        d = (C.c_int32 * (L + 1))(*dims)
+        a = (C.c_int32 * L)(*[int(x) for x in spec["act"]])
+        compute = _abi.BF16 if spec.get("compute", "f32") == "bf16" else _abi.F32
+        h = C.c_void_p()
+        check(lib().hpacml_model_create(L, d, Wp, bp, a, compute, C.byref(h)), "hpacml_model_create")
+        self.handle = h
+        self.dims = dims
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().hpacml_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return C.c_void_p(stream)
+    return C.c_void_p(stream.cuda_stream)
+
+
+def infer(model: Model, in_map: Map, out_map: Map, stream=None) -> None:
+    """``hpacml_infer``: gather -> MLP -> scatter on ``stream`` (default: torch's
+    current stream)."""
+    check(lib().hpacml_infer(model.handle, in_map.handle, out_map.handle, _stream(stream)), "hpacml_infer")
+
+
+def collect(m: Map, dst, ld: int, stream=None) -> None:
+    """``hpacml_collect`` into ``dst`` (a float32 device tensor; ``dst`` may be a
+    view offset into a larger record, e.g. ``rec[:, 9:]``)."""
+    import torch
+    if dst.dtype != torch.float32 or not dst.is_cuda:
+        raise TypeError("collect destination must be a float32 device tensor")
+    check(lib().hpacml_collect(m.handle, C.c_void_p(dst.data_ptr()), int(ld), _stream(stream)),
+          "hpacml_collect")
+
+
+def variant(model: Model, in_map: Map, out_map: Map) -> str:
+    r = lib().hpacml_infer_variant(model.handle, in_map.handle, out_map.handle)
+    return r.decode() if r else None

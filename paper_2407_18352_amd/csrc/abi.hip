@@ -1,0 +1,421 @@
+// C ABI of the library: handle management, validation and kernel dispatch.
+// Declarations and the contract of every entry point are in include/hpacml.h.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "hpacml.h"
+#include "kernels.hpp"
+#include "plan.hpp"
+
+using namespace hpacml;
+
+struct hpacml_map_s {
+    MapPlan plan;
+    int device = 0;
+    FeatureEntry *feat_dev = nullptr;
+    float **base_dev = nullptr;
+    int64_t *stride_dev = nullptr;
+    DevMap dev{};
+};
+
+enum class Variant { Generic, F32 };
+
+struct hpacml_model_s {
+    int32_t n_layers = 0, compute = 0;
+    std::vector<int32_t> dims, act;
+    int device = 0;
+    Variant variant = Variant::Generic;
+    float *gen_buf = nullptr;   // generic-kernel weights and biases
+    DevModel gen{};
+    float *f32_img = nullptr;   // packed LDS image of the fp32 kernel
+    F32Packed f32{};
+};
+
+namespace {
+
+hpacml_status hip_status(hipError_t e) {
+    if (e == hipSuccess)
+        return HPACML_OK;
+    if (e == hipErrorOutOfMemory)
+        return HPACML_E_NOMEM;
+    return HPACML_E_DEVICE;
+}
+
+// Round to bf16 (nearest even; NaN stays a quiet NaN) and back to fp32.
+float host_bf16(float x) {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) {
+        u = (u | 0x00400000u) & 0xFFFF0000u;
+    } else {
+        u += 0x7FFFu + ((u >> 16) & 1u);
+        u &= 0xFFFF0000u;
+    }
+    float r;
+    std::memcpy(&r, &u, 4);
+    return r;
+}
+
+// Every target must be device memory of the current device, and the elements
+// the map can address must lie inside that allocation.
+hpacml_status check_device_targets(const MapPlan &p, int device) {
+    for (int t = 0; t < p.n_targets; ++t) {
+        hipPointerAttribute_t attr;
+        if (hipPointerGetAttributes(&attr, p.base[t]) != hipSuccess) {
+            (void)hipGetLastError();
+            return HPACML_E_INVAL;
+        }
+        if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
+            return HPACML_E_INVAL;
+        if (attr.device != device)
+            return HPACML_E_INVAL;
+        hipDeviceptr_t abase = nullptr;
+        size_t asize = 0;
+        if (hipMemGetAddressRange(&abase, &asize, (hipDeviceptr_t)p.base[t]) != hipSuccess) {
+            (void)hipGetLastError();
+            return HPACML_E_INVAL;
+        }
+        const char *lo = (const char *)abase, *hi = lo + asize;
+        const char *a = (const char *)p.base[t];
+        if (a < lo || a + 4 * (p.max_elem[t] + 1) > hi)
+            return HPACML_E_RANGE;
+        if (((uintptr_t)a & 3u) != 0)
+            return HPACML_E_INVAL;
+    }
+    return HPACML_OK;
+}
+
+template <typename T>
+hpacml_status upload(T **dst, const T *src, size_t n) {
+    *dst = nullptr;
+    if (n == 0)
+        return HPACML_OK;
+    hipError_t e = hipMalloc((void **)dst, n * sizeof(T));
+    if (e != hipSuccess) {
+        *dst = nullptr;
+        return hip_status(e);
+    }
+    e = hipMemcpy(*dst, src, n * sizeof(T), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(*dst);
+        *dst = nullptr;
+        return hip_status(e);
+    }
+    return HPACML_OK;
+}
+
+bool same_device(int dev) {
+    int cur = -1;
+    return hipGetDevice(&cur) == hipSuccess && cur == dev;
+}
+
+hpacml_status check_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+    if (!model || !in || !out)
+        return HPACML_E_INVAL;
+    if (in->plan.dir != HPACML_TO || out->plan.dir != HPACML_FROM)
+        return HPACML_E_INVAL;
+    if (in->plan.n_points != out->plan.n_points)
+        return HPACML_E_SHAPE;
+    if (in->plan.n_features != model->dims[0] || out->plan.n_features != model->dims[model->n_layers])
+        return HPACML_E_SHAPE;
+    if (in->device != model->device || out->device != model->device || !same_device(model->device))
+        return HPACML_E_INVAL;
+    return check_alias(in->plan, out->plan);
+}
+
+}  // namespace
+
+namespace hpacml {
+
+DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev,
+                   const int64_t *stride_dev) {
+    DevMap m{};
+    m.rank = p.rank;
+    m.n_features = p.n_features;
+    m.n_targets = p.n_targets;
+    m.pointwise = p.pointwise ? 1 : 0;
+    m.n_points = p.n_points;
+    bool small = p.n_points < (int64_t(1) << 31);
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        m.count[d] = p.count[d];
+        m.start[d] = p.start[d];
+        m.step[d] = p.step[d];
+        m.extent[d] = p.extent[d];
+        m.bnd[d] = p.bnd[d];
+        m.omin[d] = p.omin[d];
+        m.omax[d] = p.omax[d];
+        m.stride0[d] = d < p.rank ? p.stride[d] : 0;
+        small = small && p.count[d] < (int64_t(1) << 31) && p.count[d] > 0;
+    }
+    m.small_counts = small ? 1 : 0;
+    m.same_strides = 1;
+    for (int t = 1; t < p.n_targets; ++t)
+        for (int d = 0; d < p.rank; ++d)
+            if (p.stride[(size_t)t * 4 + d] != p.stride[d])
+                m.same_strides = 0;
+    m.feat = feat_dev;
+    m.base = base_dev;
+    m.stride = stride_dev;
+    return m;
+}
+
+}  // namespace hpacml
+
+extern "C" {
+
+int32_t hpacml_abi_version(void) { return HPACML_ABI_VERSION; }
+
+const char *hpacml_status_string(hpacml_status s) {
+    switch (s) {
+    case HPACML_OK: return "ok";
+    case HPACML_E_INVAL: return "invalid argument";
+    case HPACML_E_SHAPE: return "shape mismatch";
+    case HPACML_E_RANGE: return "access out of range";
+    case HPACML_E_ALIAS: return "output may overwrite an input before it is read";
+    case HPACML_E_UNSUPPORTED: return "unsupported";
+    case HPACML_E_NOMEM: return "out of memory";
+    case HPACML_E_DEVICE: return "device error";
+    }
+    return "unknown status";
+}
+
+hpacml_status hpacml_map_validate(const hpacml_functor *f, int32_t dir, const hpacml_array *targets,
+                                  int32_t n_targets, const hpacml_sweep *sweep, const int32_t *bnd,
+                                  int64_t *n_points, int32_t *n_features) {
+    try {
+        MapPlan p;
+        hpacml_status s = build_map_plan(f, dir, targets, n_targets, sweep, bnd, &p);
+        if (s != HPACML_OK)
+            return s;
+        if (n_points)
+            *n_points = p.n_points;
+        if (n_features)
+            *n_features = p.n_features;
+        return HPACML_OK;
+    } catch (const std::bad_alloc &) {
+        return HPACML_E_NOMEM;
+    } catch (...) {
+        return HPACML_E_INVAL;
+    }
+}
+
+void hpacml_map_destroy(hpacml_map *m) {
+    if (!m)
+        return;
+    (void)hipFree(m->feat_dev);
+    (void)hipFree(m->base_dev);
+    (void)hipFree(m->stride_dev);
+    delete m;
+}
+
+hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir, const hpacml_array *targets,
+                                int32_t n_targets, const hpacml_sweep *sweep, const int32_t *bnd,
+                                hpacml_map **out) {
+    if (!out)
+        return HPACML_E_INVAL;
+    *out = nullptr;
+    hpacml_map *m = nullptr;
+    try {
+        m = new hpacml_map_s();
+        hpacml_status s = build_map_plan(f, dir, targets, n_targets, sweep, bnd, &m->plan);
+        if (s == HPACML_OK && hipGetDevice(&m->device) != hipSuccess) {
+            (void)hipGetLastError();
+            s = HPACML_E_DEVICE;
+        }
+        if (s == HPACML_OK)
+            s = check_device_targets(m->plan, m->device);
+        if (s == HPACML_OK)
+            s = upload(&m->feat_dev, m->plan.feat.data(), m->plan.feat.size());
+        if (s == HPACML_OK) {
+            std::vector<float *> bases(m->plan.n_targets);
+            for (int t = 0; t < m->plan.n_targets; ++t)
+                bases[t] = (float *)m->plan.base[t];
+            s = upload(&m->base_dev, bases.data(), bases.size());
+        }
+        if (s == HPACML_OK)
+            s = upload(&m->stride_dev, m->plan.stride.data(), m->plan.stride.size());
+        if (s != HPACML_OK) {
+            hpacml_map_destroy(m);
+            return s;
+        }
+        m->dev = make_devmap(m->plan, m->feat_dev, m->base_dev, m->stride_dev);
+        *out = m;
+        return HPACML_OK;
+    } catch (const std::bad_alloc &) {
+        hpacml_map_destroy(m);
+        return HPACML_E_NOMEM;
+    } catch (...) {
+        hpacml_map_destroy(m);
+        return HPACML_E_INVAL;
+    }
+}
+
+hpacml_status hpacml_map_shape(const hpacml_map *m, int64_t *n_points, int32_t *n_features) {
+    if (!m)
+        return HPACML_E_INVAL;
+    if (n_points)
+        *n_points = m->plan.n_points;
+    if (n_features)
+        *n_features = m->plan.n_features;
+    return HPACML_OK;
+}
+
+hpacml_status hpacml_model_validate(int32_t n_layers, const int32_t *dims, const int32_t *act,
+                                    int32_t compute) {
+    return validate_model(n_layers, dims, act, compute);
+}
+
+void hpacml_model_destroy(hpacml_model *m) {
+    if (!m)
+        return;
+    (void)hipFree(m->gen_buf);
+    (void)hipFree(m->f32_img);
+    delete m;
+}
+
+hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const float *const *W,
+                                  const float *const *b, const int32_t *act, int32_t compute,
+                                  hpacml_model **out) {
+    if (!out)
+        return HPACML_E_INVAL;
+    *out = nullptr;
+    hpacml_status s = validate_model(n_layers, dims, act, compute);
+    if (s != HPACML_OK)
+        return s;
+    if (!W || !b)
+        return HPACML_E_INVAL;
+    for (int l = 0; l < n_layers; ++l)
+        if (!W[l] || !b[l])
+            return HPACML_E_INVAL;
+    hpacml_model *m = nullptr;
+    try {
+        m = new hpacml_model_s();
+        m->n_layers = n_layers;
+        m->compute = compute;
+        m->dims.assign(dims, dims + n_layers + 1);
+        m->act.assign(act, act + n_layers);
+        if (hipGetDevice(&m->device) != hipSuccess) {
+            (void)hipGetLastError();
+            hpacml_model_destroy(m);
+            return HPACML_E_DEVICE;
+        }
+        const bool bf16 = compute == HPACML_BF16;
+
+        // general-shape layout: fp32 [out][in] per layer, then biases
+        std::vector<float> hostw;
+        std::vector<size_t> woff(n_layers), boff(n_layers);
+        int maxw = 1;
+        for (int l = 0; l < n_layers; ++l) {
+            woff[l] = hostw.size();
+            const size_t nw = (size_t)dims[l] * dims[l + 1];
+            for (size_t i = 0; i < nw; ++i)
+                hostw.push_back(bf16 ? host_bf16(W[l][i]) : W[l][i]);
+            boff[l] = hostw.size();
+            for (int o = 0; o < dims[l + 1]; ++o)
+                hostw.push_back(b[l][o]);
+        }
+        for (int l = 0; l <= n_layers; ++l)
+            maxw = dims[l] > maxw ? dims[l] : maxw;
+        s = upload(&m->gen_buf, hostw.data(), hostw.size());
+        if (s != HPACML_OK) {
+            hpacml_model_destroy(m);
+            return s;
+        }
+        m->gen.n_layers = n_layers;
+        m->gen.bf16 = bf16 ? 1 : 0;
+        m->gen.max_width = maxw;
+        for (int l = 0; l <= n_layers; ++l)
+            m->gen.dims[l] = dims[l];
+        for (int l = 0; l < n_layers; ++l) {
+            m->gen.act[l] = act[l];
+            m->gen.W[l] = m->gen_buf + woff[l];
+            m->gen.b[l] = m->gen_buf + boff[l];
+        }
+
+        if (f32_fast_supported(n_layers, dims, compute)) {
+            std::vector<float> img(f32_image_floats(n_layers, dims), 0.f);
+            f32_pack(n_layers, dims, W, b, img.data());
+            s = upload(&m->f32_img, img.data(), img.size());
+            if (s != HPACML_OK) {
+                hpacml_model_destroy(m);
+                return s;
+            }
+            m->f32.hid = dims[1];
+            m->f32.n_hidden = n_layers - 2;
+            m->f32.ks1 = (dims[0] + 1) / 2;
+            m->f32.f_out = dims[n_layers];
+            for (int l = 0; l < n_layers; ++l)
+                m->f32.act[l] = act[l];
+            m->f32.lds_bytes = (int32_t)(img.size() * sizeof(float));
+            m->f32.image = m->f32_img;
+            m->variant = Variant::F32;
+        }
+        *out = m;
+        return HPACML_OK;
+    } catch (const std::bad_alloc &) {
+        hpacml_model_destroy(m);
+        return HPACML_E_NOMEM;
+    } catch (...) {
+        hpacml_model_destroy(m);
+        return HPACML_E_INVAL;
+    }
+}
+
+const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+    if (check_infer(model, in, out) != HPACML_OK)
+        return nullptr;
+    switch (model->variant) {
+    case Variant::F32: return f32_variant_name(model->f32);
+    default: return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
+    }
+}
+
+hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out,
+                           void *stream) {
+    hpacml_status s = check_infer(model, in, out);
+    if (s != HPACML_OK)
+        return s;
+    if (in->plan.n_points == 0)
+        return HPACML_OK;
+    hipStream_t st = (hipStream_t)stream;
+    hipError_t e;
+    switch (model->variant) {
+    case Variant::F32: e = launch_mlp_f32(in->dev, out->dev, model->f32, st); break;
+    default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
+    }
+    return hip_status(e);
+}
+
+hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *stream) {
+    if (!m || !dst)
+        return HPACML_E_INVAL;
+    if (ld < m->plan.n_features)
+        return HPACML_E_SHAPE;
+    if (!same_device(m->device))
+        return HPACML_E_INVAL;
+    if (m->plan.n_points == 0)
+        return HPACML_OK;
+    // the record must be device memory large enough for every row
+    hipDeviceptr_t abase = nullptr;
+    size_t asize = 0;
+    if (hipMemGetAddressRange(&abase, &asize, (hipDeviceptr_t)dst) != hipSuccess) {
+        (void)hipGetLastError();
+        return HPACML_E_INVAL;
+    }
+    const int64_t need = ((m->plan.n_points - 1) * ld + m->plan.n_features) * 4;
+    if ((const char *)dst + need > (const char *)abase + asize || ((uintptr_t)dst & 3u))
+        return HPACML_E_RANGE;
+    // the record must not overlap what it reads
+    for (int t = 0; t < m->plan.n_targets; ++t) {
+        const char *a0 = (const char *)m->plan.base[t];
+        const char *a1 = a0 + 4 * (m->plan.max_elem[t] + 1);
+        if (!((const char *)dst + need <= a0 || a1 <= (const char *)dst))
+            return HPACML_E_ALIAS;
+    }
+    return hip_status(launch_collect(m->dev, reinterpret_cast<uint32_t *>(dst), ld, (hipStream_t)stream));
+}
+
+}  // extern "C"

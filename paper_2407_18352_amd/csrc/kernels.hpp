@@ -1,0 +1,49 @@
+// Kernel launchers of the library (one per kernel family).  Every launcher
+// enqueues on `stream` and returns the HIP launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "device.hpp"
+
+namespace hpacml {
+
+// Plain fp32 [out][in] weights + fp32 biases (bf16 models: values already
+// rounded to bf16), used by the general-shape kernel.
+struct DevModel {
+    int32_t n_layers;
+    int32_t bf16;
+    int32_t max_width;
+    int32_t dims[HPACML_MAX_LAYERS + 1];
+    int32_t act[HPACML_MAX_LAYERS];
+    const float *W[HPACML_MAX_LAYERS];
+    const float *b[HPACML_MAX_LAYERS];
+};
+
+// Collect: dst[p * ld + f] = bits of feature f at point p.
+hipError_t launch_collect(const DevMap &m, uint32_t *dst, int64_t ld, hipStream_t stream);
+
+// General-shape fused gather -> MLP -> scatter (VALU, any widths).
+hipError_t launch_mlp_generic(const DevMap &in, const DevMap &out, const DevModel &mdl,
+                              hipStream_t stream);
+
+// fp32 register-resident fused kernel: hidden layers of one width H in
+// {64, 128}, all weights resident in LDS, MFMA 32x32x2 f32.
+struct F32Packed {
+    int32_t hid;          // H
+    int32_t n_hidden;     // hidden-to-hidden layers (H x H), 0..6
+    int32_t ks1;          // K-steps of the first layer (ceil(F_in / 2))
+    int32_t f_out;        // outputs (1..8)
+    int32_t act[HPACML_MAX_LAYERS];
+    int32_t lds_bytes;    // size of the packed image (bytes)
+    const float *image;   // device copy of the LDS image
+};
+bool f32_fast_supported(int n_layers, const int32_t *dims, int compute);
+size_t f32_image_floats(int n_layers, const int32_t *dims);
+void f32_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
+              float *image);
+hipError_t launch_mlp_f32(const DevMap &in, const DevMap &out, const F32Packed &pk,
+                          hipStream_t stream);
+const char *f32_variant_name(const F32Packed &pk);
+
+}  // namespace hpacml

@@ -1,0 +1,67 @@
+// Host-side access plan of a tensor map (HIP-free: builds and runs on any CPU).
+//
+// The paper's data bridge turns a functor applied to a concrete sweep into
+// views of application memory in four steps (Sec. IV-A): extraction (offset
+// of each slice relative to the sweep point), resolution (element counts per
+// dimension), wrapping (views over the application arrays) and composition
+// (flatten + concatenate into the feature dimension).  The first three depend
+// only on the descriptors, so they are done here once per map; the result is a
+// per-feature table that the device kernels index directly, which makes
+// composition a gather inside the fused kernel.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "hpacml.h"
+
+namespace hpacml {
+
+// One feature of a map, as the kernels read it (32 bytes).
+struct FeatureEntry {
+    int32_t target;     // which target array
+    int32_t off[HPACML_MAX_RANK];  // offset from the sweep point, per dimension;
+                                   // periodic dims: reduced into [0, extent)
+    int32_t pad;
+    int64_t delta;      // element offset of an interior access:
+                        // sum_d raw_offset[d] * stride[target][d]
+};
+static_assert(sizeof(FeatureEntry) == 32, "FeatureEntry layout");
+
+struct MapPlan {
+    int32_t rank = 0, dir = 0, n_targets = 0, n_features = 0;
+    int64_t n_points = 0;
+    int64_t extent[HPACML_MAX_RANK] = {1, 1, 1, 1};
+    int64_t start[HPACML_MAX_RANK] = {0, 0, 0, 0};
+    int64_t step[HPACML_MAX_RANK] = {1, 1, 1, 1};
+    int64_t count[HPACML_MAX_RANK] = {1, 1, 1, 1};   // sweep points per dimension
+    int32_t bnd[HPACML_MAX_RANK] = {0, 0, 0, 0};
+    int32_t omin[HPACML_MAX_RANK] = {0, 0, 0, 0};    // raw offset range over features
+    int32_t omax[HPACML_MAX_RANK] = {0, 0, 0, 0};
+    bool pointwise = false;   // every feature reads the sweep point itself
+    bool idx32 = false;       // every element index of every target fits in int32
+    std::vector<void *> base;             // [n_targets]
+    std::vector<int64_t> stride;          // [n_targets * 4]
+    std::vector<FeatureEntry> feat;       // [n_features]
+    std::vector<int32_t> raw;             // [n_features * 4] raw offsets
+    std::vector<int64_t> max_elem;        // [n_targets] largest element index
+};
+
+// Validates a map description and builds its plan (no device calls).
+hpacml_status build_map_plan(const hpacml_functor *f, int32_t dir, const hpacml_array *targets,
+                             int32_t n_targets, const hpacml_sweep *sweep, const int32_t *bnd,
+                             MapPlan *out);
+
+// Validates a model description (no device calls).
+hpacml_status validate_model(int32_t n_layers, const int32_t *dims, const int32_t *act,
+                             int32_t compute);
+
+// Checks that inference with `in` (TO) and `out` (FROM) reads every input
+// before it can be overwritten; HPACML_E_ALIAS when a `from` target may
+// overlap a `to` target other than element-for-element at the same point.
+hpacml_status check_alias(const MapPlan &in, const MapPlan &out);
+
+// True when two targets provably address disjoint elements.
+bool disjoint_targets(const MapPlan &a, int ta, const MapPlan &b, int tb);
+
+}  // namespace hpacml

@@ -146,27 +146,45 @@ def sinusoid_field(cfg: int, k: int, ny: int, nx: int) -> np.ndarray:
     return f.astype(np.float32)
 
 
+def _normal_chunked(cfg: int, k: int, shape, workers: int) -> np.ndarray:
+    """N(0,1) float32 array drawn in slabs along axis 0, slab c from child
+    stream (cfg, k, c) (threads fill slabs in parallel)."""
+    from concurrent.futures import ThreadPoolExecutor
+    out = np.empty(shape, np.float32)
+    n0 = shape[0]
+    slabs = [(c, c * n0 // 16, (c + 1) * n0 // 16) for c in range(16)]
+
+    def fill(job):
+        c, a, b = job
+        if b > a:
+            g = np.random.Generator(np.random.PCG64(np.random.SeedSequence(ROOT_SEED, spawn_key=(cfg, k, c))))
+            g.standard_normal(out=out[a:b], dtype=np.float32)
+    with ThreadPoolExecutor(workers) as ex:
+        list(ex.map(fill, slabs))
+    return out
+
+
 def gaussian_field(cfg: int, k: int, shape, corr: float = 4.0) -> np.ndarray:
     """White N(0,1) noise filtered in Fourier space by exp(-|k|^2 corr^2 / 2),
     then standardised to zero mean and unit sample variance."""
     import scipy.fft as sfft
-    g = rng(cfg, k)
-    white = g.standard_normal(shape, dtype=np.float32)
     workers = min(16, os.cpu_count() or 1)
+    white = _normal_chunked(cfg, k, shape, workers)
     spec = sfft.rfftn(white, workers=workers)
     del white
     nz, ny, nx = shape
-    kz = (2 * np.pi * np.fft.fftfreq(nz)).astype(np.float32)[:, None, None]
-    ky = (2 * np.pi * np.fft.fftfreq(ny)).astype(np.float32)[None, :, None]
-    kx = (2 * np.pi * np.fft.rfftfreq(nx)).astype(np.float32)[None, None, :]
-    c2 = np.float32(corr * corr / 2)
-    spec *= np.exp(-(kz * kz) * c2)
-    spec *= np.exp(-(ky * ky) * c2)
-    spec *= np.exp(-(kx * kx) * c2)
-    f = sfft.irfftn(spec, s=shape, workers=workers).astype(np.float32)
+    c2 = corr * corr / 2
+    fz = np.exp(-((2 * np.pi * np.fft.fftfreq(nz)) ** 2) * c2).astype(np.float32)[:, None, None]
+    fy = np.exp(-((2 * np.pi * np.fft.fftfreq(ny)) ** 2) * c2).astype(np.float32)[None, :, None]
+    fx = np.exp(-((2 * np.pi * np.fft.rfftfreq(nx)) ** 2) * c2).astype(np.float32)[None, None, :]
+    spec *= fz
+    spec *= fy
+    spec *= fx
+    spec[0, 0, 0] = 0                      # zero mean
+    f = sfft.irfftn(spec, s=shape, workers=workers).astype(np.float32, copy=False)
     del spec
-    f -= f.mean(dtype=np.float64)
-    f /= np.float32(f.std(dtype=np.float64))
+    rms = np.sqrt(np.einsum("i,i->", f.reshape(-1), f.reshape(-1), dtype=np.float64) / f.size)
+    f *= np.float32(1.0 / rms)
     return f
 
 

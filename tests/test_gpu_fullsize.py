@@ -1,0 +1,65 @@
+"""GPU parity at the five configurations' full sizes, in the launch
+configuration the benchmark times: inference checked on a fixed seeded sample
+of rows (every grid-edge cell included) that the oracle computes one by one;
+collect indexing checked bit-exactly on whole grids (3-D: whole z-slabs that
+include the periodic wrap)."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2407_18352_amd import _abi, api
+from paper_2407_18352_amd import workloads as wl
+from gpu_util import RTOL, assert_close, require_gpu, run_collect, run_infer
+
+pytestmark = pytest.mark.gpu
+
+_cache = {}
+
+
+def full(name):
+    if name not in _cache:
+        _cache.clear()
+        _cache[name] = wl.make(name)
+    return _cache[name]
+
+
+def edges(w):
+    shape = w.inputs[0].shape
+    if len(shape) == 3:
+        return wl.edge_rows_3d(*shape)
+    if len(shape) == 2:
+        return wl.edge_rows_2d(*shape)
+    return np.array([0, shape[0] - 1], np.int64)
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+@pytest.mark.parametrize("name", wl.NAMES)
+def test_infer_fullsize_sampled(name):
+    w = full(name)
+    got, var = run_infer(w)
+    rows = wl.sample_rows(w.n_points, 2048 if name == "stencil3d" else 8192, must=edges(w))
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model, rows)
+    gotY = np.stack([a.reshape(-1)[rows] for a in got], 1)
+    worst, norm = assert_close(gotY, Y, RTOL[w.compute], "%s via %s" % (name, var))
+    print("%s [%s] full size, %d sampled rows: worst %.3e normwise %.3e" % (name, var, len(rows), worst, norm))
+    for a in got:
+        assert not np.any(a.view(np.uint32) == wl.SENTINEL_BITS), "unwritten output element"
+
+
+@pytest.mark.parametrize("name", ["options", "bonds", "stencil2d", "poses"])
+def test_collect_fullsize_bitexact(name):
+    w = full(name)
+    got = run_collect(w.in_spec, w.inputs)
+    assert np.array_equal(got, oracle.collect(w.in_spec, w.inputs))
+
+
+@pytest.mark.parametrize("z0, z1", [(0, 32), (240, 272), (480, 512)])
+def test_collect_stencil3d_slabs_bitexact(z0, z1):
+    w = full("stencil3d")
+    spec = dict(w.in_spec, sweep=((z0, 0, 0), (z1, 512, 512), (1, 1, 1)))
+    got = run_collect(spec, w.inputs)
+    assert np.array_equal(got, oracle.collect(spec, w.inputs))

@@ -1,0 +1,285 @@
+"""GPU parity: the HIP library (called through the C ABI) against the oracle.
+
+Bars: gather/scatter/collect indexing bit-exact; fp32 inference within
+|g - o| <= 1e-5 * max(|o|, s) and bf16 within 2e-2 (s = RMS of the oracle's
+output column); no NaN; untouched elements keep their sentinel bits.
+"""
+import ctypes as C
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2407_18352_amd import _abi, api
+from paper_2407_18352_amd import workloads as wl
+from gpu_util import RTOL, assert_close, require_gpu, run_collect, run_infer, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _flat_rows(arrs, rows):
+    return np.stack([a.reshape(-1)[rows] for a in arrs], axis=1)
+
+
+# ------------------------------------------------------------------ collect
+@pytest.mark.parametrize("name", wl.NAMES)
+def test_collect_small_bitexact(name):
+    w = wl.make(name, "small")
+    got = run_collect(w.in_spec, w.inputs)
+    want = oracle.collect(w.in_spec, w.inputs)
+    assert got.shape == want.shape
+    assert np.array_equal(got, want)
+
+
+def test_collect_input_output_pairs_ld():
+    """bonds: record 9 inputs + 1 output per point in one [B x 10] buffer."""
+    import torch
+    w = wl.make("bonds", "small")
+    outv = wl.rng(2, 100).uniform(0, 1, w.n_points).astype(np.float32)
+    ins, outs = to_dev(w.inputs), to_dev([outv])
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.TO)
+    rec = torch.empty((w.n_points, 10), device="cuda")
+    rec.view(torch.int32).fill_(-1)
+    api.collect(mi, rec, 10)
+    api.collect(mo, rec[:, 9:], 10)
+    torch.cuda.synchronize()
+    got = rec.cpu().numpy().view(np.uint32)
+    assert np.array_equal(got[:, :9], oracle.collect(w.in_spec, w.inputs))
+    assert np.array_equal(got[:, 9:], oracle.collect(w.out_spec, [outv]))
+
+
+def test_collect_preserves_bit_patterns_and_gaps():
+    g = np.random.default_rng(3)
+    a = g.standard_normal((33, 70)).astype(np.float32)
+    bits = a.view(np.uint32)
+    bits[0, 0], bits[1, 1], bits[2, 2] = 0x7FC0DEAD, 0x80000000, 0xFF800001
+    spec = wl.window2d_spec(33, 70)
+    got = run_collect(spec, [a], ld=13)
+    assert np.array_equal(got[:, :9], oracle.collect(spec, [a]))
+    assert np.all(got[:, 9:] == 0xFFFFFFFF)          # columns >= F untouched
+
+
+@pytest.mark.parametrize("R", [1, 2, 3])
+def test_collect_random_maps_bitexact(R):
+    """Random functors, boundary modes, steps, sub-ranges and strided views."""
+    import torch
+    g = np.random.default_rng(50 + R)
+    done = 0
+    for trial in range(40):
+        ext = [int(g.integers(1, 40 if R < 3 else 12)) for _ in range(R)]
+        bnd = [int(g.choice([wl.PERIODIC, wl.CLAMP])) for _ in range(R)]
+        slices = [(tuple(int(g.integers(-3, 4)) for _ in range(R)),
+                   tuple(int(g.integers(1, 3)) for _ in range(R))) for _ in range(int(g.integers(1, 4)))]
+        start = [int(g.integers(0, e + 1)) for e in ext]
+        stop = [int(g.integers(s, e + 1)) for s, e in zip(start, ext)]
+        step = [int(g.integers(1, 4)) for _ in range(R)]
+        spec = {"rank": R, "slices": slices, "sweep": (start, stop, step), "bnd": bnd}
+        n_t = int(g.integers(1, 4))
+        bigs = [g.standard_normal([2 * e for e in ext]).astype(np.float32) for _ in range(n_t)]
+        views = [b[tuple(slice(1, 2 * e, 2) for e in ext)] for b in bigs]
+        F = oracle.n_features(spec, views)
+        if F > 256:
+            continue
+        want = oracle.collect(spec, views)
+        dev_big = to_dev(bigs)
+        dev = [d[tuple(slice(1, 2 * e, 2) for e in ext)] for d in dev_big]
+        m = api.Map(spec, dev, _abi.TO)
+        assert (m.n_points, m.n_features) == want.shape
+        rec = torch.empty((max(1, m.n_points), F), device="cuda")
+        api.collect(m, rec, F)
+        torch.cuda.synchronize()
+        got = rec.cpu().numpy().view(np.uint32)[: m.n_points]
+        assert np.array_equal(got, want), (trial, spec)
+        m.close()
+        done += 1
+    assert done > 20
+
+
+# ------------------------------------------------------------------ infer
+@pytest.mark.parametrize("name", wl.NAMES)
+def test_infer_small(name):
+    w = wl.make(name, "small")
+    got, var = run_infer(w)
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    exp = [o.copy() for o in w.outputs]
+    oracle.scatter(w.out_spec, exp, Y)
+    gotY = np.stack([a.reshape(-1) for a in got], 1)
+    expY = np.stack([a.reshape(-1) for a in exp], 1)
+    worst, norm = assert_close(gotY, expY, RTOL[w.compute], "%s via %s" % (name, var))
+    print("%s [%s]: worst %.3e normwise %.3e" % (name, var, worst, norm))
+
+
+def test_infer_fp32_fast_path_is_used():
+    for name, want in [("options", "mlp_f32_h64"), ("bonds", "mlp_f32_h128"), ("stencil2d", "mlp_f32_h128")]:
+        w = wl.make(name, 1000 if name != "stencil2d" else (20, 40))
+        _, var = run_infer(w)
+        assert var.startswith(want), (name, var)
+
+
+def _one_hot_chain(F_in, H, n_hidden, pick, compute):
+    """Layer 1 copies input i to hidden unit i; hidden layers copy unit o to
+    unit o; the output layer picks input `pick`.  Exact on non-negative inputs."""
+    dims = [F_in] + [H] * (n_hidden + 1) + [1]
+    W, b = [], []
+    W1 = np.zeros((H, F_in), np.float32)
+    W1[np.arange(F_in), np.arange(F_in)] = 1
+    W.append(W1)
+    for _ in range(n_hidden):
+        W.append(np.eye(H, dtype=np.float32))
+    Wo = np.zeros((1, H), np.float32)
+    Wo[0, pick] = 1
+    W.append(Wo)
+    b = [np.zeros(d, np.float32) for d in dims[1:]]
+    return {"dims": dims, "W": W, "b": b, "act": [1] * (n_hidden + 1) + [0], "compute": compute}
+
+
+@pytest.mark.parametrize("H, n_hidden, compute", [(64, 1, "f32"), (128, 2, "f32"), (128, 1, "f32"),
+                                                  (256, 2, "bf16"), (512, 1, "bf16"), (96, 1, "f32")])
+def test_one_hot_chain_bitexact(H, n_hidden, compute):
+    w = wl.make("bonds", 4099)
+    for pick in (0, 4, 8):
+        w.model = _one_hot_chain(9, H, n_hidden, pick, compute)
+        w.outputs = [wl.sentinel_like((4099,))]
+        got, var = run_infer(w)
+        x = w.inputs[pick]
+        if compute == "bf16":
+            x = oracle.bf16_bits(x).astype(np.uint32) << 16
+            x = x.view(np.float32)
+        assert np.array_equal(got[0].view(np.uint32), x.view(np.uint32)), (pick, var)
+
+
+def test_guard_band_and_subsweep():
+    """A strided sub-sweep writes exactly its points; everything else keeps the
+    sentinel bits."""
+    ny, nx = 61, 133
+    w = wl.make("stencil2d", (ny, nx))
+    sweep = ((3, 5), (58, 120), (2, 3))
+    w.in_spec = dict(w.in_spec, sweep=sweep)
+    w.out_spec = dict(w.out_spec, sweep=sweep)
+    got, var = run_infer(w)
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    exp = [o.copy() for o in w.outputs]
+    oracle.scatter(w.out_spec, exp, Y)
+    mask = np.zeros((ny, nx), bool)
+    mask[3:58:2, 5:120:3] = True
+    for g in range(4):
+        assert np.array_equal(got[g][~mask].view(np.uint32), exp[g][~mask].view(np.uint32))
+        assert not np.any(got[g][mask].view(np.uint32) == wl.SENTINEL_BITS)
+    assert_close(np.stack([a[mask] for a in got], 1), Y, RTOL["f32"], var)
+
+
+def test_determinism_and_batch_order():
+    """Same inputs twice -> identical bits; a shifted sub-sweep (other tile
+    alignment) gives the same bits for the shared points."""
+    w = wl.make("bonds", 9001)
+    a, _ = run_infer(w)
+    b, _ = run_infer(w)
+    assert np.array_equal(a[0].view(np.uint32), b[0].view(np.uint32))
+    w2 = wl.make("bonds", 9001)
+    w2.in_spec = dict(w2.in_spec, sweep=((13,), (9001,), (1,)))
+    w2.out_spec = dict(w2.out_spec, sweep=((13,), (9001,), (1,)))
+    c, _ = run_infer(w2)
+    assert np.array_equal(c[0][13:].view(np.uint32), a[0][13:].view(np.uint32))
+
+
+@pytest.mark.parametrize("compute", ["f32", "bf16"])
+def test_generic_shapes_rank3_clamp_strided(compute):
+    """Shapes outside the MFMA kernels: uneven widths, rank-3 clamp/periodic
+    map with steps, strided target views."""
+    import torch
+    g = np.random.default_rng(77)
+    shape = (9, 11, 14)
+    spec = {"rank": 3, "slices": [((-1, 0, 0), (3, 1, 1)), ((0, -2, 1), (1, 2, 2))],
+            "sweep": ((1, 0, 2), (9, 11, 13), (2, 1, 3)), "bnd": [wl.CLAMP, wl.PERIODIC, wl.CLAMP]}
+    bigs = [g.standard_normal((9, 11, 28)).astype(np.float32) for _ in range(2)]
+    views = [b[:, :, ::2] for b in bigs]
+    F = oracle.n_features(spec, views)
+    dims = [F, 40, 24, 3]
+    model = wl.make_model(9, dims, compute)
+    npts = oracle.n_points(spec, views)
+    outs_np = [wl.sentinel_like((npts,)) for _ in range(3)]
+    Y = oracle.infer_rows(spec, views, model)
+    dev = [d[:, :, ::2] for d in to_dev(bigs)]
+    outs = to_dev(outs_np)
+    mi = api.Map(spec, dev, _abi.TO)
+    mo = api.Map(wl.pointwise_spec(npts), outs, _abi.FROM)
+    m = api.Model(model)
+    assert api.variant(m, mi, mo).startswith("mlp_generic")
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    got = np.stack([o.cpu().numpy() for o in outs], 1)
+    assert_close(got, Y, RTOL[compute], "generic " + compute)
+
+
+# ------------------------------------------------------------------ errors
+def test_errors_are_reported_before_launch():
+    import torch
+    w = wl.make("bonds", 1000)
+    ins, outs = to_dev(w.inputs), to_dev(w.outputs)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.FROM)
+    model = api.Model(w.model)
+    # host memory is not a device pointer
+    host = [torch.from_numpy(a) for a in w.inputs]
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.Map(w.in_spec, host, _abi.TO)
+    assert e.value.status == _abi.E_INVAL
+    # point-count mismatch
+    short = api.Map(wl.pointwise_spec(999), [o[:999] for o in outs], _abi.FROM)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.infer(model, mi, short)
+    assert e.value.status == _abi.E_SHAPE
+    # wrong direction
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.infer(model, mo, mi)
+    assert e.value.status == _abi.E_INVAL
+    # an output overlapping an input other than element-for-element
+    shifted = api.Map(dict(wl.pointwise_spec(999)), [ins[0][1:]], _abi.FROM)
+    mi999 = api.Map(wl.pointwise_spec(999), [x[:999] for x in ins], _abi.TO)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.infer(model, mi999, shifted)
+    assert e.value.status == _abi.E_ALIAS
+    # element-for-element in place is allowed
+    inplace = api.Map(w.out_spec, [ins[3]], _abi.FROM)
+    api.infer(model, mi, inplace)
+    torch.cuda.synchronize()
+    # a record too small for every row
+    rec = torch.empty((999, 9), device="cuda")
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.collect(mi, rec, 9)
+    assert e.value.status == _abi.E_RANGE
+    # extents beyond the allocation (1 GiB view of a 400-byte tensor)
+    t = torch.zeros(100, device="cuda")
+    L = _abi.lib()
+    n_big = 1 << 28
+    f, keep = api._functor(wl.pointwise_spec(n_big), 1)
+    sw, bnd = api._sweep(wl.pointwise_spec(n_big))
+    arr = (_abi.Array * 1)(api.array_desc(t.data_ptr(), (n_big,), (1,)))
+    h = C.c_void_p()
+    assert L.hpacml_map_create(C.byref(f), _abi.TO, arr, 1, C.byref(sw), bnd, C.byref(h)) == _abi.E_RANGE
+    assert h.value is None
+    # zero points: OK, nothing launched
+    e0 = api.Map({"rank": 1, "slices": [((0,), (1,))], "sweep": ((5,), (5,), (1,)), "bnd": [0]},
+                 [ins[0]], _abi.TO)
+    assert e0.n_points == 0
+    api.collect(e0, rec, 9)
+
+
+def test_inplace_pointwise_matches_oracle():
+    """Element-for-element in-place update: the output overwrites input 0."""
+    import torch
+    w = wl.make("options", 5000)
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    ins = to_dev(w.inputs)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, [ins[0]], _abi.FROM)
+    m = api.Model(w.model)
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    assert_close(ins[0].cpu().numpy()[:, None], Y, RTOL["f32"], "in place")
