@@ -249,11 +249,19 @@ def test_errors_are_reported_before_launch():
     inplace = api.Map(w.out_spec, [ins[3]], _abi.FROM)
     api.infer(model, mi, inplace)
     torch.cuda.synchronize()
-    # a record too small for every row
+    # a record leading dimension that runs past the end of the allocation
     rec = torch.empty((999, 9), device="cuda")
     with pytest.raises(_abi.HpacmlError) as e:
-        api.collect(mi, rec, 9)
+        api.collect(mi, rec, 1 << 22)
     assert e.value.status == _abi.E_RANGE
+    # ld smaller than the feature count
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.collect(mi, rec, 8)
+    assert e.value.status == _abi.E_SHAPE
+    # a record overlapping a mapped input
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.collect(mi, ins[0][:90].view(10, 9), 9)
+    assert e.value.status in (_abi.E_ALIAS, _abi.E_RANGE)
     # extents beyond the allocation (1 GiB view of a 400-byte tensor)
     t = torch.zeros(100, device="cuda")
     L = _abi.lib()
