@@ -3,14 +3,21 @@
 
 One step = one pass of the whole hot path over the workload: the fused
 gather -> MLP -> scatter (``hpacml_infer``) plus the collect records of the
-region's inputs and outputs (``hpacml_collect`` twice into one [B x (F_in +
-F_out)] buffer).  Inputs are synthetic, seeded and resident in HBM before the
-timed region.  Prints one JSON line.
+region's inputs and outputs (``hpacml_collect`` into a [B x F_in] input
+record and a [B x F_out] output record, the two datasets a collected region
+stores).  Inputs are synthetic, seeded and resident in HBM before the timed
+region.  Prints one JSON line.
+
+``roofline.traffic`` is the HBM traffic per launch of the dominant kernel
+from the committed rocprofv3 counter summary in ``profiles/``, used only while
+the kernel's source hash still matches the one recorded there (else null).
 
 Default workload: bond-pricing surrogate, 1,048,576 points, 9 SoA fp32 inputs,
 MLP 9 -> 128 -> 128 -> 128 -> 1 (ReLU), fp32.
 """
 import argparse
+import glob
+import hashlib
 import json
 import os
 import sys
@@ -33,6 +40,36 @@ DESCRIPTION = {
     "stencil3d": "3-D stencil: 512^3 grid x 5 fp32 fields, periodic 7-point window (35 features), "
                  "MLP 35-512-512-5 ReLU, bf16 with fp32 accumulate, 5 outputs per cell",
 }
+
+
+KERNEL_SOURCES = {
+    "mlp_f32": ["mlp_f32.hip", "device.hpp", "kernels.hpp"],
+    "mlp_bf16": ["mlp_bf16.hip", "device.hpp", "kernels.hpp"],
+    "mlp_generic": ["mlp_generic.hip", "device.hpp", "kernels.hpp"],
+}
+
+
+def recorded_traffic(variant):
+    """HBM bytes per launch of `variant` from profiles/*.txt, if the kernel
+    source is unchanged since the counters were taken."""
+    fam = next((k for k in KERNEL_SOURCES if variant.startswith(k)), None)
+    if fam is None:
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[fam]:
+        path = os.path.join(ROOT, "paper_2407_18352_amd", "csrc", f)
+        if not os.path.exists(path):
+            return None
+        h.update(open(path, "rb").read())
+    sha = h.hexdigest()[:16]
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.txt"))):
+        for line in open(path):
+            if line.startswith("traffic_line ") and ("kernel=%s " % variant) in line:
+                kv = dict(t.split("=", 1) for t in line.split()[1:])
+                if kv.get("source_sha256") == sha:
+                    return {"bytes": int(kv["bytes"]), "fetch": int(kv["fetch"]), "write": int(kv["write"]),
+                            "source": os.path.relpath(path, ROOT)}
+    return None
 
 
 def main():
@@ -75,8 +112,8 @@ def main():
     model = api.Model(w.model)
     variant = api.variant(model, mi, mo)
     B, Fi, Fo = mi.n_points, mi.n_features, mo.n_features
-    ld = Fi + Fo
-    rec = torch.empty((B, ld), device="cuda")
+    rec_in = torch.empty((B, Fi), device="cuda")
+    rec_out = torch.empty((B, Fo), device="cuda")
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -85,8 +122,8 @@ def main():
         api.infer(model, mi, mo, stream)
         if ev is not None:
             ev[1].record(stream)
-        api.collect(mi, rec, ld, stream)
-        api.collect(mo_rec, rec[:, Fi:], ld, stream)
+        api.collect(mi, rec_in, Fi, stream)
+        api.collect(mo_rec, rec_out, Fo, stream)
 
     if args.copy_calibration_mb:
         src = torch.empty(args.copy_calibration_mb << 18, device="cuda")
@@ -117,6 +154,7 @@ def main():
     flops_pt = w.flops_per_point
     achieved = flops_pt * B / (infer_avg * 1e-3)
     peak = PEAK[w.compute]
+    traffic = recorded_traffic(variant)
     result = {
         "metric": "surrogate points/sec (gather+MLP+scatter) and % of HBM / MFMA roofline",
         "value": B / (ms_step * 1e-3),
@@ -133,7 +171,9 @@ def main():
         "config": {"workload": DESCRIPTION[args.workload], "points": B, "features_in": Fi,
                    "features_out": Fo, "dims": w.dims, "kernel": variant},
         "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
+                     "frac": achieved / peak, "traffic": traffic["bytes"] if traffic else None,
+                     "traffic_source": traffic["source"] if traffic else None,
+                     "algorithmic_hbm_bytes_per_launch": w.hbm_bytes_per_point * B,
                      "kernel": variant, "kernel_avg_ms": infer_avg,
                      "algorithmic_flop_per_launch": flops_pt * B},
         "infer_points_per_s": B / (infer_avg * 1e-3),
