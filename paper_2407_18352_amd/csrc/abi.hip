@@ -21,7 +21,7 @@ struct hpacml_map_s {
     DevMap dev{};
 };
 
-enum class Variant { Generic, F32 };
+enum class Variant { Generic, F32, BF16 };
 
 struct hpacml_model_s {
     int32_t n_layers = 0, compute = 0;
@@ -32,6 +32,9 @@ struct hpacml_model_s {
     DevModel gen{};
     float *f32_img = nullptr;   // packed LDS image of the fp32 kernel
     F32Packed f32{};
+    uint16_t *bf16_frags = nullptr;  // packed fragments of the bf16 kernel
+    float *bf16_bias = nullptr;
+    BF16Packed bf16{};
 };
 
 namespace {
@@ -273,6 +276,8 @@ void hpacml_model_destroy(hpacml_model *m) {
         return;
     (void)hipFree(m->gen_buf);
     (void)hipFree(m->f32_img);
+    (void)hipFree(m->bf16_frags);
+    (void)hipFree(m->bf16_bias);
     delete m;
 }
 
@@ -352,6 +357,25 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
             m->f32.lds_bytes = (int32_t)(img.size() * sizeof(float));
             m->f32.image = m->f32_img;
             m->variant = Variant::F32;
+        } else if (bf16_fast_supported(n_layers, dims, compute)) {
+            std::vector<uint16_t> frags;
+            std::vector<float> b1, bh;
+            bf16_pack(n_layers, dims, W, b, frags, b1, bh, &m->bf16);
+            std::vector<float> biases(b1);
+            biases.insert(biases.end(), bh.begin(), bh.end());
+            s = upload(&m->bf16_frags, frags.data(), frags.size());
+            if (s == HPACML_OK)
+                s = upload(&m->bf16_bias, biases.data(), biases.size());
+            if (s != HPACML_OK) {
+                hpacml_model_destroy(m);
+                return s;
+            }
+            for (int l = 0; l < n_layers; ++l)
+                m->bf16.act[l] = act[l];
+            m->bf16.frags = m->bf16_frags;
+            m->bf16.bias1 = m->bf16_bias;
+            m->bf16.biash = m->bf16_bias + b1.size();
+            m->variant = Variant::BF16;
         }
         *out = m;
         return HPACML_OK;
@@ -369,6 +393,7 @@ const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in
         return nullptr;
     switch (model->variant) {
     case Variant::F32: return f32_variant_name(model->f32);
+    case Variant::BF16: return bf16_variant_name(model->bf16);
     default: return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
     }
 }
@@ -384,6 +409,7 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
     hipError_t e;
     switch (model->variant) {
     case Variant::F32: e = launch_mlp_f32(in->dev, out->dev, model->f32, st); break;
+    case Variant::BF16: e = launch_mlp_bf16(in->dev, out->dev, model->bf16, st); break;
     default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
     }
     return hip_status(e);

@@ -4,6 +4,9 @@
 
 #include <hip/hip_runtime.h>
 
+#include <cstring>
+#include <vector>
+
 #include "device.hpp"
 
 namespace hpacml {
@@ -45,5 +48,28 @@ void f32_pack(int n_layers, const int32_t *dims, const float *const *W, const fl
 hipError_t launch_mlp_f32(const DevMap &in, const DevMap &out, const F32Packed &pk,
                           hipStream_t stream);
 const char *f32_variant_name(const F32Packed &pk);
+
+// bf16 fused kernel: hidden layers of one width H in {256, 512}; activations
+// in LDS, weights streamed from L2 as prepacked MFMA fragments.
+struct BF16Packed {
+    int32_t hid;          // H
+    int32_t n_hidden;     // hidden-to-hidden layers (H x H)
+    int32_t ks1;          // 16-wide K-steps of the first layer (F_in <= 64)
+    int32_t f_out;        // outputs (1..16)
+    int32_t act[HPACML_MAX_LAYERS];
+    int64_t off_w1, off_wh, off_wo;   // fragment offsets, 16-byte units
+    uint32_t frag_bytes;  // size of the packed fragments
+    const void *frags;    // device: packed bf16 fragments
+    const float *bias1;   // device: first-layer bias, C-fragment order
+    const float *biash;   // device: hidden-layer biases, C-fragment order
+    float bias_out[16];
+};
+bool bf16_fast_supported(int n_layers, const int32_t *dims, int compute);
+size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
+                 std::vector<uint16_t> &frags, std::vector<float> &bias1, std::vector<float> &biash,
+                 BF16Packed *pk);
+hipError_t launch_mlp_bf16(const DevMap &in, const DevMap &out, const BF16Packed &pk,
+                           hipStream_t stream);
+const char *bf16_variant_name(const BF16Packed &pk);
 
 }  // namespace hpacml

@@ -1,0 +1,399 @@
+// bf16 fused region kernel: gather -> MLP -> scatter for wide hidden layers
+// (H in {256, 512}), bf16 operands with fp32 accumulation on
+// v_mfma_f32_32x32x16_bf16 (hidden layers) and v_mfma_f32_16x16x32_bf16
+// (output layer).
+//
+// The surrogate runs per sweep point on the composed input tensor
+// (Sec. IV-A composition, Sec. IV-B inference).  The hidden weights of these
+// models (128 KB - 512 KB per layer in bf16) do not fit in LDS, so the roles
+// are the reverse of the fp32 kernel: a block of 8 waves (2 per SIMD) owns a
+// tile of T points (T * H = 65536) whose activations sit in LDS as bf16
+// [T][H] (128 KB), and the weights stream from L2 straight into MFMA A
+// fragments (prepacked so each fragment is one 16-byte load per lane).  Every
+// layer is H_out^T = W * H_in^T; each wave computes a 64-feature x 128-point
+// block, so each weight fragment fetched from L2 feeds 4 MFMAs and each
+// activation fragment read from LDS feeds 2.  Per layer: zero-initialised
+// fp32 accumulators (128 per lane), the K loop (A from L2, B from LDS), a
+// block barrier, then the epilogue adds the bias, applies the activation,
+// rounds to bf16 and stores over the layer's input.  Two waves per SIMD let
+// one wave's epilogue overlap the other's MFMAs.
+//
+// LDS rows are sequences of 16-byte chunks (8 bf16).  The epilogue stores the
+// 16 values a lane holds for one (m-block, point) as two chunks; the order of
+// features inside a chunk is fixed by the MFMA C layout, and the next layer's
+// weight columns are permuted to match when the weights are packed.  Rows are
+// padded by one chunk, so the 8 lanes (8 consecutive points) that share an
+// LDS cycle hit distinct banks, and every address is a per-lane base plus a
+// compile-time offset.
+#include "kernels.hpp"
+
+namespace hpacml {
+
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kThreads = 512;   // 8 waves, 2 per SIMD
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Raw buffer view of the packed weights: loads take a per-lane byte offset
+// plus a wave-uniform offset, so the K loop keeps no per-step 64-bit
+// addresses in VGPRs; accesses past `bytes` read zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t weight_rsrc(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ uint4 wload(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+    __bf16 x = (__bf16)a, y = (__bf16)b;
+    return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+}
+
+// feature held at element e of LDS chunk c (C layout of the 32x32 MFMA,
+// two chunks per (m-block, lane half))
+__host__ __device__ inline int chunk_feature(int c, int e) {
+    return 32 * (c / 4) + 16 * ((c % 4) / 2) + 8 * (e / 4) + 4 * (c % 2) + (e % 4);
+}
+
+// Bias of m-blocks m0, m0+1 in C-fragment order: lane half g, register r of
+// m-block m holds bias[32m + 8(r/4) + 4g + r%4].
+__device__ __forceinline__ void load_bias2(const float *bias, int m0, int g, floatx16 *bf) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const uint4 *bp = reinterpret_cast<const uint4 *>(bias) + ((m0 + j) * 2 + g) * 4;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint4 u = bp[q];
+            bf[j][4 * q + 0] = __builtin_bit_cast(float, u.x);
+            bf[j][4 * q + 1] = __builtin_bit_cast(float, u.y);
+            bf[j][4 * q + 2] = __builtin_bit_cast(float, u.z);
+            bf[j][4 * q + 3] = __builtin_bit_cast(float, u.w);
+        }
+    }
+}
+
+// Tile geometry: 8 waves in a WM x WN grid; every wave computes a 64-feature
+// x 128-point block (2 x 4 MFMA blocks, 128 fp32 accumulators per lane).
+template <int H>
+struct Geo {
+    static constexpr int T = 65536 / H;          // points per tile
+    static constexpr int NMB = H / 32;           // 32-row m-blocks per layer
+    static constexpr int WM = H / 64;            // waves along features
+    static constexpr int WN = 8 / WM;            // waves along points
+    static constexpr int KS = H / 16;            // K-steps of a hidden layer
+    static constexpr int RC = H / 8;             // chunks per activation row
+    static constexpr int PH = RC + 1;            // row pitch in chunks (padded)
+    static constexpr int NB16 = T / 128;         // 16-point n-blocks per wave (output layer)
+    static_assert(T / WN == 128, "wave tile is 128 points");
+};
+
+template <int H, int KS1MAX>
+__global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap out, BF16Packed pk,
+                                                            int64_t n_tiles) {
+    using G = Geo<H>;
+    constexpr int PX = 2 * KS1MAX + 1;             // gathered-input row pitch (chunks)
+    extern __shared__ uint4 smem[];
+    uint4 *Hs = smem;                              // [T][PH] activations
+    uint4 *Xs = smem + G::T * G::PH;               // [T][PX] gathered inputs
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int wm = w % G::WM, wn = w / G::WM;
+    const int g = lane >> 5;
+    const int col = lane & 31;
+    const int m0 = 2 * wm;                         // first m-block of this wave
+    const int p0 = 128 * wn + col;                 // this lane's point in n-block 0
+    const int F = in.n_features;
+    const int nchunk_in = 2 * pk.ks1;              // chunks the first layer reads
+    const __amdgpu_buffer_rsrc_t wr = weight_rsrc(pk.frags, pk.frag_bytes);
+    const uint32_t vlane = (uint32_t)((m0 * 64 + lane) * 16);
+    const floatx16 zero = {};
+
+    // XCD-aware tile order: blocks on one XCD take adjacent tiles
+    const int nb = gridDim.x;
+    const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
+
+    for (int64_t tile = lb; tile < n_tiles; tile += nb) {
+        const int64_t b0 = tile * G::T;
+
+        // ---- gather: (point, chunk) pairs, 8 features per chunk, rounded to bf16
+        for (int idx = tid; idx < G::T * nchunk_in; idx += kThreads) {
+            const int p = idx % G::T, c = idx / G::T;
+            const int64_t b = b0 + p;
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                v[e] = 0.f;
+            if (b < in.n_points && 8 * c < F) {
+                int64_t pt[HPACML_MAX_RANK];
+                sweep_point(in, b, pt);
+                const bool inside = interior(in, pt);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int f = 8 * c + e;
+                    if (f < F)
+                        v[e] = *feature_ptr(in, pt, inside, f);
+                }
+            }
+            uint4 q;
+            q.x = pack2(v[0], v[1]);
+            q.y = pack2(v[2], v[3]);
+            q.z = pack2(v[4], v[5]);
+            q.w = pack2(v[6], v[7]);
+            Xs[p * PX + c] = q;
+        }
+        __syncthreads();
+
+        floatx16 acc[2][4];
+
+        // ---- first layer: A = W1 fragments, B = gathered inputs (LDS);
+        //      accumulators start from zero (the bias is added in the epilogue)
+#pragma unroll
+        for (int s = 0; s < KS1MAX; ++s) {
+            if (s < pk.ks1) {
+                uint4 a[2];
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    a[j] = wload(wr, vlane + j * 1024, (uint32_t)((pk.off_w1 + (int64_t)s * G::NMB * 64) * 16));
+#pragma unroll
+                for (int n = 0; n < 4; ++n) {
+                    const bf16x8 bv = as_bf16x8(Xs[(p0 + 32 * n) * PX + 2 * s + g]);
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[j]), bv,
+                                                                             s == 0 ? zero : acc[j][n], 0, 0, 0);
+                }
+            }
+        }
+
+        // ---- hidden layers: epilogue of the previous layer (bias, activation,
+        //      bf16 into LDS), then H x H
+        for (int h = 0; h <= pk.n_hidden; ++h) {
+            const bool relu = pk.act[h] == HPACML_ACT_RELU;
+            floatx16 bf[2];
+            load_bias2(h == 0 ? pk.bias1 : pk.biash + (size_t)(h - 1) * G::NMB * 32, m0, g, bf);
+            __syncthreads();               // every wave is done reading Hs
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+#pragma unroll
+                for (int n = 0; n < 4; ++n) {
+#pragma unroll
+                    for (int sp = 0; sp < 2; ++sp) {
+                        float v[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) {
+                            const float x = acc[j][n][8 * sp + e] + bf[j][8 * sp + e];
+                            v[e] = relu ? fmaxf(x, 0.f) : x;
+                        }
+                        uint4 q;
+                        q.x = pack2(v[0], v[1]);
+                        q.y = pack2(v[2], v[3]);
+                        q.z = pack2(v[4], v[5]);
+                        q.w = pack2(v[6], v[7]);
+                        Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = q;
+                    }
+                }
+            }
+            __syncthreads();               // the layer's activations are complete
+            if (h == pk.n_hidden)
+                break;
+
+            // K loop, fully unrolled; scheduling barriers pin the pipeline:
+            // weight fragments two K-steps ahead (ring of 4), activation
+            // fragments one K-step ahead (ring of 2)
+            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * G::KS * G::NMB * 64) * 16);
+            uint4 A[4][2];
+            uint4 Bq[2][4];
+            auto load_a = [&](uint4 *dst, int s) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    dst[j] = wload(wr, vlane + j * 1024, wbase + (uint32_t)s * G::NMB * 1024);
+            };
+            auto load_b = [&](uint4 *dst, int s) {
+#pragma unroll
+                for (int n = 0; n < 4; ++n)
+                    dst[n] = Hs[(p0 + 32 * n) * G::PH + 2 * s + g];
+            };
+            load_a(A[0], 0);
+            load_a(A[1], 1);
+            load_b(Bq[0], 0);
+#pragma unroll
+            for (int s = 0; s < G::KS; ++s) {
+                if (s + 2 < G::KS)
+                    load_a(A[(s + 2) & 3], s + 2);
+                if (s + 1 < G::KS)
+                    load_b(Bq[(s + 1) & 1], s + 1);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int n = 0; n < 4; ++n) {
+                    const bf16x8 bv = as_bf16x8(Bq[s & 1][n]);
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(A[s & 3][j]), bv,
+                                                                             s == 0 ? zero : acc[j][n], 0, 0, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+
+        // ---- output layer: 16 x T, K = H on 16x16x32; wave w takes points
+        //      [w*T/8, (w+1)*T/8); lane (l%16 = point, l/16 = k group)
+        {
+            const int q = lane >> 4, pc = lane & 15;
+            floatx4 y[G::NB16];
+#pragma unroll
+            for (int s = 0; s < H / 32; ++s) {
+                const uint4 a = wload(wr, (uint32_t)(lane * 16), (uint32_t)((pk.off_wo + (int64_t)s * 64) * 16));
+#pragma unroll
+                for (int n = 0; n < G::NB16; ++n) {
+                    const int p = w * (G::T / 8) + 16 * n + pc;
+                    const bf16x8 bv = as_bf16x8(Hs[p * G::PH + 4 * s + q]);
+                    y[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), bv, s == 0 ? floatx4{} : y[n],
+                                                                    0, 0, 0);
+                }
+            }
+            const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
+#pragma unroll
+            for (int n = 0; n < G::NB16; ++n) {
+                const int p = w * (G::T / 8) + 16 * n + pc;
+                const int64_t b = b0 + p;
+                if (b >= out.n_points)
+                    continue;
+                int64_t pt[HPACML_MAX_RANK];
+                sweep_point(out, b, pt);
+                const bool inside = interior(out, pt);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int go = 4 * q + r;
+                    if (go < pk.f_out) {
+                        float v = y[n][r] + pk.bias_out[go];
+                        if (orelu)
+                            v = fmaxf(v, 0.f);
+                        *const_cast<float *>(feature_ptr(out, pt, inside, go)) = v;
+                    }
+                }
+            }
+        }
+        // the next tile's gather writes Xs only: no wave reads Xs past the
+        // first layer, and Hs is not written again before a barrier
+    }
+}
+
+template <int H, int KS1MAX>
+hipError_t launch_t(const DevMap &in, const DevMap &out, const BF16Packed &pk, hipStream_t stream) {
+    using G = Geo<H>;
+    const int64_t n_tiles = (in.n_points + G::T - 1) / G::T;
+    const size_t lds = (size_t)G::T * (G::PH + 2 * KS1MAX + 1) * 16;
+    int64_t grid = n_tiles < 256 ? n_tiles : 256;
+    auto kern = mlp_bf16_kernel<H, KS1MAX>;
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, stream, in, out, pk, n_tiles);
+    return hipGetLastError();
+}
+
+uint16_t bf16_bits_host(float x) {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u)
+        return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+}  // namespace
+
+bool bf16_fast_supported(int n_layers, const int32_t *dims, int compute) {
+    if (compute != HPACML_BF16 || n_layers < 2 || n_layers > HPACML_MAX_LAYERS)
+        return false;
+    const int H = dims[1];
+    if (H != 256 && H != 512)
+        return false;
+    for (int l = 1; l < n_layers; ++l)
+        if (dims[l] != H)
+            return false;
+    // the gathered-input rows share the 160 KB of LDS with the activations
+    return dims[0] <= (H == 512 ? 64 : 32) && dims[n_layers] <= 16;
+}
+
+// Packed layout (uint16 units):
+//   W1 fragments [ks1][NMB][64 lanes][8]    A[i=l%32][k=8(l/32)+e] = W1[32m+i][16s+k]
+//   hidden       [n_hidden][KS][NMB][64][8] columns permuted to the LDS chunk order
+//   output       [H/32][64][8]              A[i=l%16][k=8(l/16)+e] (16x16x32 layout)
+// followed by fp32 biases in C-fragment order.
+size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
+                 std::vector<uint16_t> &frags, std::vector<float> &bias1, std::vector<float> &biash,
+                 BF16Packed *pk) {
+    const int H = dims[1], Fin = dims[0], Fout = dims[n_layers];
+    const int NMB = H / 32, KS = H / 16, ks1 = (Fin + 15) / 16;
+    const int n_hidden = n_layers - 2;
+    frags.clear();
+    pk->off_w1 = 0;
+    for (int s = 0; s < ks1; ++s)
+        for (int m = 0; m < NMB; ++m)
+            for (int l = 0; l < 64; ++l)
+                for (int e = 0; e < 8; ++e) {
+                    const int o = 32 * m + l % 32, k = 16 * s + 8 * (l / 32) + e;
+                    frags.push_back(k < Fin ? bf16_bits_host(W[0][(size_t)o * Fin + k]) : 0);
+                }
+    pk->off_wh = (int64_t)(frags.size() / 8);
+    for (int h = 0; h < n_hidden; ++h)
+        for (int s = 0; s < KS; ++s)
+            for (int m = 0; m < NMB; ++m)
+                for (int l = 0; l < 64; ++l)
+                    for (int e = 0; e < 8; ++e) {
+                        const int o = 32 * m + l % 32;
+                        const int k = chunk_feature(2 * s + l / 32, e);
+                        frags.push_back(bf16_bits_host(W[h + 1][(size_t)o * H + k]));
+                    }
+    pk->off_wo = (int64_t)(frags.size() / 8);
+    for (int s = 0; s < H / 32; ++s)
+        for (int l = 0; l < 64; ++l)
+            for (int e = 0; e < 8; ++e) {
+                const int i = l % 16;
+                const int k = chunk_feature(4 * s + l / 16, e);
+                frags.push_back(i < Fout ? bf16_bits_host(W[n_layers - 1][(size_t)i * H + k]) : 0);
+            }
+    auto cbias = [&](const float *bb, std::vector<float> &dst) {
+        for (int m = 0; m < NMB; ++m)
+            for (int g = 0; g < 2; ++g)
+                for (int r = 0; r < 16; ++r)
+                    dst.push_back(bb[32 * m + 8 * (r / 4) + 4 * g + (r % 4)]);
+    };
+    bias1.clear();
+    biash.clear();
+    cbias(b[0], bias1);
+    for (int h = 0; h < n_hidden; ++h)
+        cbias(b[h + 1], biash);
+    if (biash.empty())
+        biash.push_back(0.f);
+    pk->frag_bytes = (uint32_t)(frags.size() * 2);
+    pk->hid = H;
+    pk->n_hidden = n_hidden;
+    pk->ks1 = ks1;
+    pk->f_out = Fout;
+    for (int i = 0; i < 16; ++i)
+        pk->bias_out[i] = i < Fout ? b[n_layers - 1][i] : 0.f;
+    return frags.size();
+}
+
+hipError_t launch_mlp_bf16(const DevMap &in, const DevMap &out, const BF16Packed &pk, hipStream_t stream) {
+    if (in.n_points == 0)
+        return hipSuccess;
+    if (pk.hid == 512)
+        return pk.ks1 <= 1 ? launch_t<512, 1>(in, out, pk, stream) : launch_t<512, 4>(in, out, pk, stream);
+    return pk.ks1 <= 1 ? launch_t<256, 1>(in, out, pk, stream) : launch_t<256, 2>(in, out, pk, stream);
+}
+
+const char *bf16_variant_name(const BF16Packed &pk) {
+    return pk.hid == 512 ? "mlp_bf16_h512" : "mlp_bf16_h256";
+}
+
+}  // namespace hpacml

@@ -115,9 +115,10 @@ def test_infer_small(name):
     print("%s [%s]: worst %.3e normwise %.3e" % (name, var, worst, norm))
 
 
-def test_infer_fp32_fast_path_is_used():
-    for name, want in [("options", "mlp_f32_h64"), ("bonds", "mlp_f32_h128"), ("stencil2d", "mlp_f32_h128")]:
-        w = wl.make(name, 1000 if name != "stencil2d" else (20, 40))
+def test_infer_fast_paths_are_used():
+    for name, want in [("options", "mlp_f32_h64"), ("bonds", "mlp_f32_h128"), ("stencil2d", "mlp_f32_h128"),
+                       ("poses", "mlp_bf16_h256"), ("stencil3d", "mlp_bf16_h512")]:
+        w = wl.make(name, {"stencil2d": (20, 40), "stencil3d": (6, 7, 9)}.get(name, 1000))
         _, var = run_infer(w)
         assert var.startswith(want), (name, var)
 
