@@ -19,6 +19,8 @@ struct hpacml_map_s {
     float **base_dev = nullptr;
     int64_t *stride_dev = nullptr;
     DevMap dev{};
+    Map32 m32{};
+    bool fast = false;   // m32 is valid
 };
 
 enum class Variant { Generic, F32, BF16 };
@@ -33,7 +35,6 @@ struct hpacml_model_s {
     float *f32_img = nullptr;   // packed LDS image of the fp32 kernel
     F32Packed f32{};
     uint16_t *bf16_frags = nullptr;  // packed fragments of the bf16 kernel
-    float *bf16_bias = nullptr;
     BF16Packed bf16{};
 };
 
@@ -165,6 +166,57 @@ DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const 
     return m;
 }
 
+bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev, Map32 *out) {
+    const int64_t lim = INT32_MAX;
+    Map32 m{};
+    if (p.n_points >= lim || !p.idx32)
+        return false;
+    for (int t = 1; t < p.n_targets; ++t)
+        for (int d = 0; d < p.rank; ++d)
+            if (p.stride[(size_t)t * 4 + d] != p.stride[d])
+                return false;
+    for (const FeatureEntry &e : p.feat)
+        if (e.delta > lim || e.delta < -lim)
+            return false;
+    m.rank = p.rank;
+    m.n_features = p.n_features;
+    m.n_targets = p.n_targets;
+    m.n_points = (int32_t)p.n_points;
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        const bool used = d < p.rank;
+        if (used && (p.count[d] < 1 || p.start[d] + p.count[d] * p.step[d] > 2 * lim / 3 ||
+                     p.extent[d] > lim / 3 || p.stride[d] > lim || p.omin[d] < -lim / 3 || p.omax[d] > lim / 3))
+            return false;
+        m.count[d] = used ? (int32_t)p.count[d] : 1;
+        m.start[d] = used ? (int32_t)p.start[d] : 0;
+        m.step[d] = used ? (int32_t)p.step[d] : 1;
+        m.extent[d] = used ? (int32_t)p.extent[d] : 1;
+        m.stride[d] = used ? (int32_t)p.stride[d] : 0;
+        m.bnd[d] = p.bnd[d];
+        m.omin[d] = p.omin[d];
+        m.omax[d] = p.omax[d];
+        // n / d == (n * magic) >> (31 + l) for n < 2^31, l = ceil(log2 d)
+        const uint64_t dv = (uint64_t)m.count[d];
+        int l = 0;
+        while ((uint64_t(1) << l) < dv)
+            ++l;
+        const uint64_t magic = ((uint64_t(1) << (31 + l)) + dv - 1) / dv;
+        if (magic > UINT32_MAX)
+            return false;
+        m.magic[d] = (uint32_t)magic;
+        m.shift[d] = 31 + l;
+        const uint32_t probes[6] = {0u, (uint32_t)dv - 1u, (uint32_t)dv, (uint32_t)(2 * dv - 1),
+                                    (uint32_t)INT32_MAX, (uint32_t)INT32_MAX - 1u};
+        for (uint32_t n : probes)
+            if ((uint32_t)(((uint64_t)n * m.magic[d]) >> m.shift[d]) != n / (uint32_t)dv)
+                return false;
+    }
+    m.feat = feat_dev;
+    m.base = base_dev;
+    *out = m;
+    return true;
+}
+
 }  // namespace hpacml
 
 extern "C" {
@@ -245,6 +297,7 @@ hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir, const hpac
             return s;
         }
         m->dev = make_devmap(m->plan, m->feat_dev, m->base_dev, m->stride_dev);
+        m->fast = make_map32(m->plan, m->feat_dev, m->base_dev, &m->m32);
         *out = m;
         return HPACML_OK;
     } catch (const std::bad_alloc &) {
@@ -277,7 +330,6 @@ void hpacml_model_destroy(hpacml_model *m) {
     (void)hipFree(m->gen_buf);
     (void)hipFree(m->f32_img);
     (void)hipFree(m->bf16_frags);
-    (void)hipFree(m->bf16_bias);
     delete m;
 }
 
@@ -359,13 +411,8 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
             m->variant = Variant::F32;
         } else if (bf16_fast_supported(n_layers, dims, compute)) {
             std::vector<uint16_t> frags;
-            std::vector<float> b1, bh;
-            bf16_pack(n_layers, dims, W, b, frags, b1, bh, &m->bf16);
-            std::vector<float> biases(b1);
-            biases.insert(biases.end(), bh.begin(), bh.end());
+            bf16_pack(n_layers, dims, W, b, frags, &m->bf16);
             s = upload(&m->bf16_frags, frags.data(), frags.size());
-            if (s == HPACML_OK)
-                s = upload(&m->bf16_bias, biases.data(), biases.size());
             if (s != HPACML_OK) {
                 hpacml_model_destroy(m);
                 return s;
@@ -373,8 +420,6 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
             for (int l = 0; l < n_layers; ++l)
                 m->bf16.act[l] = act[l];
             m->bf16.frags = m->bf16_frags;
-            m->bf16.bias1 = m->bf16_bias;
-            m->bf16.biash = m->bf16_bias + b1.size();
             m->variant = Variant::BF16;
         }
         *out = m;
@@ -391,7 +436,8 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
 const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
     if (check_infer(model, in, out) != HPACML_OK)
         return nullptr;
-    switch (model->variant) {
+    const bool fast = in->fast && out->fast;
+    switch (fast ? model->variant : Variant::Generic) {
     case Variant::F32: return f32_variant_name(model->f32);
     case Variant::BF16: return bf16_variant_name(model->bf16);
     default: return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
@@ -407,9 +453,10 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
         return HPACML_OK;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
-    switch (model->variant) {
-    case Variant::F32: e = launch_mlp_f32(in->dev, out->dev, model->f32, st); break;
-    case Variant::BF16: e = launch_mlp_bf16(in->dev, out->dev, model->bf16, st); break;
+    const bool fast = in->fast && out->fast;
+    switch (fast ? model->variant : Variant::Generic) {
+    case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, model->f32, st); break;
+    case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, model->bf16, st); break;
     default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
     }
     return hip_status(e);

@@ -18,6 +18,9 @@ constexpr int kBatch = 8;
 __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__restrict__ dst,
                                                       int64_t ld, int pitch, int64_t n_tiles) {
     extern __shared__ uint32_t tile[];
+    __shared__ LdsPlan<HPACML_MAX_FEATURES, HPACML_MAX_TARGETS> plan;
+    plan.stage(m);
+    __syncthreads();
     const int F = m.n_features;
     const int P = blockDim.x;                  // points per tile (one per thread)
     const int t = threadIdx.x;
@@ -30,17 +33,19 @@ __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__rest
         const int64_t b = b0 + t;
         const bool valid = b < m.n_points;
         int64_t p[HPACML_MAX_RANK];
-        sweep_point(m, valid ? b : 0, p);
+        sweep_point(m, valid ? b : m.n_points - 1, p);
         const bool inside = interior(m, p);
+        const int64_t pe = point_elem(m, p, 0);
 
+        // feature-uniform batches; loads unconditional (feature numbers
+        // clamped) so a batch has all its loads in flight at once
         for (int fb = 0; fb < F; fb += kBatch) {
             uint32_t v[kBatch];
 #pragma unroll
             for (int k = 0; k < kBatch; ++k) {
-                const int f = fb + k;
-                v[k] = 0;
-                if (f < F && valid)
-                    v[k] = *reinterpret_cast<const uint32_t *>(feature_ptr(m, p, inside, f));
+                const int f = fb + k < F ? fb + k : F - 1;
+                const FeatureEntry e = plan.feat[f];
+                v[k] = ldg_bits(plan.base[e.target] + gather_elem(m, p, inside, pe, e));
             }
 #pragma unroll
             for (int k = 0; k < kBatch; ++k)

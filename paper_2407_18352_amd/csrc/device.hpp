@@ -28,6 +28,17 @@ struct DevMap {
     int64_t stride0[HPACML_MAX_RANK];  // strides of target 0
 };
 
+// Load / store of application data through the global address space: a
+// pointer fetched from LDS is generic, and a generic (flat) access counts
+// against the LDS counter as well, which would serialise a run of gathers.
+__device__ __forceinline__ float ldg(const float *p) {
+    return *(const __attribute__((address_space(1))) float *)p;
+}
+__device__ __forceinline__ uint32_t ldg_bits(const float *p) {
+    return *(const __attribute__((address_space(1))) uint32_t *)p;
+}
+__device__ __forceinline__ void stg(float *p, float v) { *(__attribute__((address_space(1))) float *)p = v; }
+
 // Sweep point of row b (row-major over the sweep counts).
 __device__ __forceinline__ void sweep_point(const DevMap &m, int64_t b, int64_t p[HPACML_MAX_RANK]) {
 #pragma unroll
@@ -91,6 +102,31 @@ __device__ __forceinline__ int64_t resolved_elem(const DevMap &m, const int64_t 
     return idx;
 }
 
+// Element index of feature e at sweep point p, free of divergent branches so
+// that a run of gathers issues all its loads before the first wait: the
+// interior form (point element + precomputed offset) and the boundary-
+// resolved form are both computed and selected per lane.  `pe` is the
+// point's element index in target 0 (used when all targets share strides).
+__device__ __forceinline__ int64_t gather_elem(const DevMap &m, const int64_t p[HPACML_MAX_RANK], bool inside,
+                                               int64_t pe, const FeatureEntry &e) {
+    int64_t res = 0, pt = 0;
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        if (d < m.rank) {
+            const int64_t n = m.extent[d];
+            const int64_t st = m.same_strides ? m.stride0[d] : m.stride[e.target * 4 + d];
+            const int64_t q = p[d] + e.off[d];
+            const int64_t qp = q >= n ? q - n : q;                    // off reduced into [0, n)
+            const int64_t qc = q < 0 ? 0 : (q >= n ? n - 1 : q);
+            const int64_t r = m.bnd[d] == HPACML_BND_PERIODIC ? qp : (m.bnd[d] == HPACML_BND_CLAMP ? qc : q);
+            res += r * st;
+            pt += p[d] * st;
+        }
+    }
+    const int64_t in = (m.same_strides ? pe : pt) + e.delta;
+    return inside ? in : res;
+}
+
 // Address of feature f of the point at row b, given its sweep point p.
 __device__ __forceinline__ const float *feature_ptr(const DevMap &m, const int64_t p[HPACML_MAX_RANK],
                                                     bool inside, int f) {
@@ -105,7 +141,91 @@ __device__ __forceinline__ float round_bf16(float x) {
     return (float)h;
 }
 
+// 32-bit view of a map for the MFMA kernels.  Valid when the point count,
+// every sweep count and every element index fit in int32 and all targets
+// share strides (the common case); maps outside it take the general kernel.
+// Division by the sweep counts uses precomputed multipliers: for n < 2^31,
+// n / d == (n * magic) >> shift with shift = 31 + ceil(log2 d) and
+// magic = ceil(2^shift / d).
+struct Map32 {
+    int32_t rank, n_features, n_targets, n_points;
+    int32_t count[HPACML_MAX_RANK], start[HPACML_MAX_RANK], step[HPACML_MAX_RANK];
+    int32_t extent[HPACML_MAX_RANK], stride[HPACML_MAX_RANK];
+    int32_t bnd[HPACML_MAX_RANK], omin[HPACML_MAX_RANK], omax[HPACML_MAX_RANK];
+    uint32_t magic[HPACML_MAX_RANK];
+    int32_t shift[HPACML_MAX_RANK];
+    const FeatureEntry *feat;          // device
+    float *const *base;                // device
+};
+
+// A sweep point resolved for gathering: coordinates, element index in the
+// (shared) strides, and whether every feature's access stays inside.
+struct Pt32 {
+    int32_t p[HPACML_MAX_RANK];
+    int32_t pe;
+    bool inside;
+};
+
+__device__ __forceinline__ Pt32 locate32(const Map32 &m, int32_t b) {
+    Pt32 r;
+    uint32_t rem = (uint32_t)b;
+    r.pe = 0;
+    r.inside = true;
+#pragma unroll
+    for (int d = HPACML_MAX_RANK - 1; d >= 0; --d) {
+        if (d < m.rank) {
+            const uint32_t q = (uint32_t)(((uint64_t)rem * m.magic[d]) >> m.shift[d]);
+            const int32_t k = (int32_t)(rem - q * (uint32_t)m.count[d]);
+            rem = q;
+            const int32_t x = m.start[d] + k * m.step[d];
+            r.p[d] = x;
+            r.pe += x * m.stride[d];
+            r.inside = r.inside && (x + m.omin[d] >= 0) && (x + m.omax[d] < m.extent[d]);
+        } else {
+            r.p[d] = 0;
+        }
+    }
+    return r;
+}
+
+// Element index of feature e at point r with boundary resolution, free of
+// divergent branches (both forms computed and selected per lane).
+__device__ __forceinline__ int32_t elem32(const Map32 &m, const Pt32 &r, const FeatureEntry &e) {
+    int32_t res = 0;
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        if (d < m.rank) {
+            const int32_t n = m.extent[d];
+            const int32_t q = r.p[d] + e.off[d];
+            const int32_t qp = q >= n ? q - n : q;                    // off reduced into [0, n)
+            const int32_t qc = q < 0 ? 0 : (q >= n ? n - 1 : q);
+            const int32_t rr = m.bnd[d] == HPACML_BND_PERIODIC ? qp : (m.bnd[d] == HPACML_BND_CLAMP ? qc : q);
+            res += rr * m.stride[d];
+        }
+    }
+    return r.inside ? r.pe + (int32_t)e.delta : res;
+}
+
+// Per-block LDS copy of the parts of a plan that the gathers index with a
+// wave-uniform feature number: read from LDS they cost no vector-memory
+// counter slots, so the data loads that follow can all be in flight at once.
+template <int NF, int NT>
+struct LdsPlan {
+    FeatureEntry feat[NF];
+    float *base[NT];
+    // cooperative copy by the whole block; call __syncthreads() after
+    template <typename M>
+    __device__ void stage(const M &m) {
+        for (int i = threadIdx.x; i < m.n_features && i < NF; i += blockDim.x)
+            feat[i] = m.feat[i];
+        for (int i = threadIdx.x; i < m.n_targets && i < NT; i += blockDim.x)
+            base[i] = m.base[i];
+    }
+};
+
 __host__ DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev,
                             const int64_t *stride_dev);
+// Fills `out` and returns true when the map fits the 32-bit view.
+__host__ bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev, Map32 *out);
 
 }  // namespace hpacml

@@ -45,7 +45,7 @@ bool f32_fast_supported(int n_layers, const int32_t *dims, int compute);
 size_t f32_image_floats(int n_layers, const int32_t *dims);
 void f32_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
               float *image);
-hipError_t launch_mlp_f32(const DevMap &in, const DevMap &out, const F32Packed &pk,
+hipError_t launch_mlp_f32(const Map32 &in, const Map32 &out, const F32Packed &pk,
                           hipStream_t stream);
 const char *f32_variant_name(const F32Packed &pk);
 
@@ -59,16 +59,13 @@ struct BF16Packed {
     int32_t act[HPACML_MAX_LAYERS];
     int64_t off_w1, off_wh, off_wo;   // fragment offsets, 16-byte units
     uint32_t frag_bytes;  // size of the packed fragments
-    const void *frags;    // device: packed bf16 fragments
-    const float *bias1;   // device: first-layer bias, C-fragment order
-    const float *biash;   // device: hidden-layer biases, C-fragment order
+    const void *frags;    // device: packed bf16 fragments (biases folded in)
     float bias_out[16];
 };
 bool bf16_fast_supported(int n_layers, const int32_t *dims, int compute);
 size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
-                 std::vector<uint16_t> &frags, std::vector<float> &bias1, std::vector<float> &biash,
-                 BF16Packed *pk);
-hipError_t launch_mlp_bf16(const DevMap &in, const DevMap &out, const BF16Packed &pk,
+                 std::vector<uint16_t> &frags, BF16Packed *pk);
+hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const BF16Packed &pk,
                            hipStream_t stream);
 const char *bf16_variant_name(const BF16Packed &pk);
 

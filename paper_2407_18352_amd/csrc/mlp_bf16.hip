@@ -1,7 +1,7 @@
 // bf16 fused region kernel: gather -> MLP -> scatter for wide hidden layers
 // (H in {256, 512}), bf16 operands with fp32 accumulation on
-// v_mfma_f32_32x32x16_bf16 (hidden layers) and v_mfma_f32_16x16x32_bf16
-// (output layer).
+// v_mfma_f32_32x32x16_bf16 (first and hidden layers) and
+// v_mfma_f32_16x16x32_bf16 (output layer).
 //
 // The surrogate runs per sweep point on the composed input tensor
 // (Sec. IV-A composition, Sec. IV-B inference).  The hidden weights of these
@@ -12,19 +12,24 @@
 // fragments (prepacked so each fragment is one 16-byte load per lane).  Every
 // layer is H_out^T = W * H_in^T; each wave computes a 64-feature x 128-point
 // block, so each weight fragment fetched from L2 feeds 4 MFMAs and each
-// activation fragment read from LDS feeds 2.  Per layer: zero-initialised
-// fp32 accumulators (128 per lane), the K loop (A from L2, B from LDS), a
-// block barrier, then the epilogue adds the bias, applies the activation,
-// rounds to bf16 and stores over the layer's input.  Two waves per SIMD let
-// one wave's epilogue overlap the other's MFMAs.
+// activation fragment read from LDS feeds 2.  Per layer: the K loop (A from
+// L2, B from LDS) into 128 fp32 accumulators per lane, a block barrier, then
+// the epilogue applies the activation, rounds to bf16 and stores over the
+// layer's input.
+//
+// Biases ride in the K dimension: each activation row carries a constant
+// chunk [1, 1, 1, 0, ...] and the weight fragments of one extra K-step hold
+// the fp32 bias split exactly into three bf16 terms (hi + mid + lo), so the
+// MFMA accumulates the bias and the epilogue is activation + conversion only.
+// The first layer uses spare columns of its zero-padded K the same way.
 //
 // LDS rows are sequences of 16-byte chunks (8 bf16).  The epilogue stores the
 // 16 values a lane holds for one (m-block, point) as two chunks; the order of
 // features inside a chunk is fixed by the MFMA C layout, and the next layer's
 // weight columns are permuted to match when the weights are packed.  Rows are
-// padded by one chunk, so the 8 lanes (8 consecutive points) that share an
-// LDS cycle hit distinct banks, and every address is a per-lane base plus a
-// compile-time offset.
+// padded to an odd number of chunks, so the 8 lanes (8 consecutive points)
+// that share an LDS cycle hit distinct banks, and every address is a per-lane
+// base plus a compile-time offset.
 #include "kernels.hpp"
 
 namespace hpacml {
@@ -33,7 +38,9 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 512;   // 8 waves, 2 per SIMD
 
@@ -50,32 +57,25 @@ __device__ __forceinline__ uint4 wload(__amdgpu_buffer_rsrc_t r, uint32_t voff, 
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
+// two fp32 -> packed bf16 pair (round to nearest even), one instruction
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-    __bf16 x = (__bf16)a, y = (__bf16)b;
-    return (uint32_t)__builtin_bit_cast(uint16_t, x) | ((uint32_t)__builtin_bit_cast(uint16_t, y) << 16);
+    const floatx2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__device__ __forceinline__ uint4 pack8(const float *v) {
+    uint4 q;
+    q.x = pack2(v[0], v[1]);
+    q.y = pack2(v[2], v[3]);
+    q.z = pack2(v[4], v[5]);
+    q.w = pack2(v[6], v[7]);
+    return q;
 }
 
 // feature held at element e of LDS chunk c (C layout of the 32x32 MFMA,
 // two chunks per (m-block, lane half))
 __host__ __device__ inline int chunk_feature(int c, int e) {
     return 32 * (c / 4) + 16 * ((c % 4) / 2) + 8 * (e / 4) + 4 * (c % 2) + (e % 4);
-}
-
-// Bias of m-blocks m0, m0+1 in C-fragment order: lane half g, register r of
-// m-block m holds bias[32m + 8(r/4) + 4g + r%4].
-__device__ __forceinline__ void load_bias2(const float *bias, int m0, int g, floatx16 *bf) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const uint4 *bp = reinterpret_cast<const uint4 *>(bias) + ((m0 + j) * 2 + g) * 4;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const uint4 u = bp[q];
-            bf[j][4 * q + 0] = __builtin_bit_cast(float, u.x);
-            bf[j][4 * q + 1] = __builtin_bit_cast(float, u.y);
-            bf[j][4 * q + 2] = __builtin_bit_cast(float, u.z);
-            bf[j][4 * q + 3] = __builtin_bit_cast(float, u.w);
-        }
-    }
 }
 
 // Tile geometry: 8 waves in a WM x WN grid; every wave computes a 64-feature
@@ -86,16 +86,16 @@ struct Geo {
     static constexpr int NMB = H / 32;           // 32-row m-blocks per layer
     static constexpr int WM = H / 64;            // waves along features
     static constexpr int WN = 8 / WM;            // waves along points
-    static constexpr int KS = H / 16;            // K-steps of a hidden layer
-    static constexpr int RC = H / 8;             // chunks per activation row
-    static constexpr int PH = RC + 1;            // row pitch in chunks (padded)
+    static constexpr int KS = H / 16;            // K-steps of a hidden layer (plus one for the bias)
+    static constexpr int RC = H / 8;             // chunks of activations per row
+    static constexpr int PH = RC + 3;            // row pitch: activations, bias chunk, zero chunk, pad
     static constexpr int NB16 = T / 128;         // 16-point n-blocks per wave (output layer)
     static_assert(T / WN == 128, "wave tile is 128 points");
 };
 
 template <int H, int KS1MAX>
-__global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap out, BF16Packed pk,
-                                                            int64_t n_tiles) {
+__global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out, BF16Packed pk,
+                                                            int32_t n_tiles) {
     using G = Geo<H>;
     constexpr int PX = 2 * KS1MAX + 1;             // gathered-input row pitch (chunks)
     extern __shared__ uint4 smem[];
@@ -113,47 +113,73 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
     const int nchunk_in = 2 * pk.ks1;              // chunks the first layer reads
     const __amdgpu_buffer_rsrc_t wr = weight_rsrc(pk.frags, pk.frag_bytes);
     const uint32_t vlane = (uint32_t)((m0 * 64 + lane) * 16);
-    const floatx16 zero = {};
+
+    __shared__ LdsPlan<64, 64> pin;                // F_in <= 64 features
+    __shared__ LdsPlan<16, 16> pout;               // F_out <= 16
+    pin.stage(in);
+    pout.stage(out);
+    // constant chunks of every activation row: [1,1,1,0,...] then zeros
+    for (int r = tid; r < G::T; r += kThreads) {
+        const float one3[8] = {1.f, 1.f, 1.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        Hs[r * G::PH + G::RC] = pack8(one3);
+        Hs[r * G::PH + G::RC + 1] = uint4{0u, 0u, 0u, 0u};
+    }
+    __syncthreads();
 
     // XCD-aware tile order: blocks on one XCD take adjacent tiles
     const int nb = gridDim.x;
     const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
 
-    for (int64_t tile = lb; tile < n_tiles; tile += nb) {
-        const int64_t b0 = tile * G::T;
+    for (int tile = lb; tile < n_tiles; tile += nb) {
+        const int b0 = tile * G::T;
 
-        // ---- gather: (point, chunk) pairs, 8 features per chunk, rounded to bf16
-        for (int idx = tid; idx < G::T * nchunk_in; idx += kThreads) {
-            const int p = idx % G::T, c = idx / G::T;
-            const int64_t b = b0 + p;
-            float v[8];
+        // ---- gather: (point, chunk) pairs, 8 features per chunk, rounded to
+        //      bf16; features F..F+2 are the constant 1 that carries the
+        //      first-layer bias.  Every pass of a thread has the same point
+        //      (the block size is a multiple of T), so its sweep point is
+        //      resolved once; T is a multiple of 64, so the chunk is
+        //      wave-uniform.  Loads are unconditional (feature numbers clamped
+        //      into the plan; unused values replaced afterwards), so all of
+        //      them are in flight before the first use.
+        {
+            constexpr int PASSES = (G::T * 2 * KS1MAX + kThreads - 1) / kThreads;
+            const int p = tid % G::T;
+            const int b = b0 + p;
+            const bool valid = b < in.n_points;
+            const Pt32 pt = locate32(in, valid ? b : in.n_points - 1);
+            const bool fast = __all(pt.inside);          // no boundary resolution anywhere
+            float v[PASSES][8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-                v[e] = 0.f;
-            if (b < in.n_points && 8 * c < F) {
-                int64_t pt[HPACML_MAX_RANK];
-                sweep_point(in, b, pt);
-                const bool inside = interior(in, pt);
+            for (int it = 0; it < PASSES; ++it) {
+                int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
+                c = c < nchunk_in ? c : nchunk_in - 1;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int f = 8 * c + e < F ? 8 * c + e : F - 1;
+                    const FeatureEntry fe = pin.feat[f];
+                    const int32_t idx = fast ? pt.pe + (int32_t)fe.delta : elem32(in, pt, fe);
+                    v[it][e] = ldg(pin.base[fe.target] + idx);
+                }
+            }
+#pragma unroll
+            for (int it = 0; it < PASSES; ++it) {
+                const int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
+                float u[8];
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const int f = 8 * c + e;
-                    if (f < F)
-                        v[e] = *feature_ptr(in, pt, inside, f);
+                    u[e] = f < F ? (valid ? v[it][e] : 0.f) : (f < F + 3 ? 1.f : 0.f);
                 }
+                if (c < nchunk_in)
+                    Xs[p * PX + c] = pack8(u);
             }
-            uint4 q;
-            q.x = pack2(v[0], v[1]);
-            q.y = pack2(v[2], v[3]);
-            q.z = pack2(v[4], v[5]);
-            q.w = pack2(v[6], v[7]);
-            Xs[p * PX + c] = q;
         }
         __syncthreads();
 
         floatx16 acc[2][4];
 
-        // ---- first layer: A = W1 fragments, B = gathered inputs (LDS);
-        //      accumulators start from zero (the bias is added in the epilogue)
+        // ---- first layer: A = W1 fragments (bias in columns F..F+2), B =
+        //      gathered inputs (LDS); accumulators start from zero
 #pragma unroll
         for (int s = 0; s < KS1MAX; ++s) {
             if (s < pk.ks1) {
@@ -166,39 +192,42 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
                     const bf16x8 bv = as_bf16x8(Xs[(p0 + 32 * n) * PX + 2 * s + g]);
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
-                        acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a[j]), bv,
-                                                                             s == 0 ? zero : acc[j][n], 0, 0, 0);
+                        acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            as_bf16x8(a[j]), bv, s == 0 ? floatx16{} : acc[j][n], 0, 0, 0);
                 }
             }
         }
 
-        // ---- hidden layers: epilogue of the previous layer (bias, activation,
-        //      bf16 into LDS), then H x H
+        // ---- hidden layers: epilogue of the previous layer (activation,
+        //      bf16 into LDS), then H x H plus the bias K-step
         for (int h = 0; h <= pk.n_hidden; ++h) {
-            const bool relu = pk.act[h] == HPACML_ACT_RELU;
-            floatx16 bf[2];
-            load_bias2(h == 0 ? pk.bias1 : pk.biash + (size_t)(h - 1) * G::NMB * 32, m0, g, bf);
             __syncthreads();               // every wave is done reading Hs
+            if (pk.act[h] == HPACML_ACT_RELU) {
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
+                for (int j = 0; j < 2; ++j)
 #pragma unroll
-                for (int n = 0; n < 4; ++n) {
+                    for (int n = 0; n < 4; ++n)
 #pragma unroll
-                    for (int sp = 0; sp < 2; ++sp) {
-                        float v[8];
+                        for (int sp = 0; sp < 2; ++sp) {
+                            float v[8];
 #pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const float x = acc[j][n][8 * sp + e] + bf[j][8 * sp + e];
-                            v[e] = relu ? fmaxf(x, 0.f) : x;
+                            for (int e = 0; e < 8; ++e)
+                                v[e] = fmaxf(acc[j][n][8 * sp + e], 0.f);
+                            Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = pack8(v);
                         }
-                        uint4 q;
-                        q.x = pack2(v[0], v[1]);
-                        q.y = pack2(v[2], v[3]);
-                        q.z = pack2(v[4], v[5]);
-                        q.w = pack2(v[6], v[7]);
-                        Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = q;
-                    }
-                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+#pragma unroll
+                    for (int n = 0; n < 4; ++n)
+#pragma unroll
+                        for (int sp = 0; sp < 2; ++sp) {
+                            float v[8];
+#pragma unroll
+                            for (int e = 0; e < 8; ++e)
+                                v[e] = acc[j][n][8 * sp + e];
+                            Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = pack8(v);
+                        }
             }
             __syncthreads();               // the layer's activations are complete
             if (h == pk.n_hidden)
@@ -207,7 +236,8 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
             // K loop, fully unrolled; scheduling barriers pin the pipeline:
             // weight fragments two K-steps ahead (ring of 4), activation
             // fragments one K-step ahead (ring of 2)
-            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * G::KS * G::NMB * 64) * 16);
+            constexpr int KT = G::KS + 1;
+            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * KT * G::NMB * 64) * 16);
             uint4 A[4][2];
             uint4 Bq[2][4];
             auto load_a = [&](uint4 *dst, int s) {
@@ -224,10 +254,10 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
             load_a(A[1], 1);
             load_b(Bq[0], 0);
 #pragma unroll
-            for (int s = 0; s < G::KS; ++s) {
-                if (s + 2 < G::KS)
+            for (int s = 0; s < KT; ++s) {
+                if (s + 2 < KT)
                     load_a(A[(s + 2) & 3], s + 2);
-                if (s + 1 < G::KS)
+                if (s + 1 < KT)
                     load_b(Bq[(s + 1) & 1], s + 1);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -235,8 +265,8 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
                     const bf16x8 bv = as_bf16x8(Bq[s & 1][n]);
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
-                        acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(A[s & 3][j]), bv,
-                                                                             s == 0 ? zero : acc[j][n], 0, 0, 0);
+                        acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            as_bf16x8(A[s & 3][j]), bv, s == 0 ? floatx16{} : acc[j][n], 0, 0, 0);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -262,20 +292,17 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
 #pragma unroll
             for (int n = 0; n < G::NB16; ++n) {
                 const int p = w * (G::T / 8) + 16 * n + pc;
-                const int64_t b = b0 + p;
-                if (b >= out.n_points)
-                    continue;
-                int64_t pt[HPACML_MAX_RANK];
-                sweep_point(out, b, pt);
-                const bool inside = interior(out, pt);
+                const int b = b0 + p;
+                const Pt32 pt = locate32(out, b < out.n_points ? b : out.n_points - 1);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int go = 4 * q + r;
-                    if (go < pk.f_out) {
+                    if (go < pk.f_out && b < out.n_points) {
                         float v = y[n][r] + pk.bias_out[go];
                         if (orelu)
                             v = fmaxf(v, 0.f);
-                        *const_cast<float *>(feature_ptr(out, pt, inside, go)) = v;
+                        const FeatureEntry fe = pout.feat[go];
+                        stg(pout.base[fe.target] + elem32(out, pt, fe), v);
                     }
                 }
             }
@@ -286,11 +313,11 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(DevMap in, DevMap ou
 }
 
 template <int H, int KS1MAX>
-hipError_t launch_t(const DevMap &in, const DevMap &out, const BF16Packed &pk, hipStream_t stream) {
+hipError_t launch_t(const Map32 &in, const Map32 &out, const BF16Packed &pk, hipStream_t stream) {
     using G = Geo<H>;
-    const int64_t n_tiles = (in.n_points + G::T - 1) / G::T;
+    const int32_t n_tiles = (in.n_points + G::T - 1) / G::T;
     const size_t lds = (size_t)G::T * (G::PH + 2 * KS1MAX + 1) * 16;
-    int64_t grid = n_tiles < 256 ? n_tiles : 256;
+    const int32_t grid = n_tiles < 256 ? n_tiles : 256;
     auto kern = mlp_bf16_kernel<H, KS1MAX>;
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
@@ -299,13 +326,34 @@ hipError_t launch_t(const DevMap &in, const DevMap &out, const BF16Packed &pk, h
     return hipGetLastError();
 }
 
-uint16_t bf16_bits_host(float x) {
+uint16_t bf16_rne_host(float x) {
     uint32_t u;
     std::memcpy(&u, &x, 4);
     if ((u & 0x7FFFFFFFu) > 0x7F800000u)
         return (uint16_t)((u >> 16) | 0x40u);
     u += 0x7FFFu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
+}
+
+float bf16_value(uint16_t h) {
+    const uint32_t u = (uint32_t)h << 16;
+    float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// fp32 bias as three bf16 terms with hi + mid + lo == b exactly: hi and mid
+// keep the leading 8 significant bits of b and of b - hi (truncation, so the
+// differences stay exact), lo the last 8.
+void split_bias(float b, uint16_t out[3]) {
+    uint32_t u;
+    std::memcpy(&u, &b, 4);
+    out[0] = (uint16_t)(u >> 16);
+    const float r1 = b - bf16_value(out[0]);
+    std::memcpy(&u, &r1, 4);
+    out[1] = (uint16_t)(u >> 16);
+    const float r2 = r1 - bf16_value(out[1]);
+    out[2] = bf16_rne_host(r2);
 }
 
 }  // namespace
@@ -319,20 +367,21 @@ bool bf16_fast_supported(int n_layers, const int32_t *dims, int compute) {
     for (int l = 1; l < n_layers; ++l)
         if (dims[l] != H)
             return false;
-    // the gathered-input rows share the 160 KB of LDS with the activations
-    return dims[0] <= (H == 512 ? 64 : 32) && dims[n_layers] <= 16;
+    // the gathered-input rows (F_in + 3 bias columns) share the 160 KB of LDS
+    // with the activations
+    return dims[0] + 3 <= (H == 512 ? 64 : 16) && dims[n_layers] <= 16;
 }
 
 // Packed layout (uint16 units):
-//   W1 fragments [ks1][NMB][64 lanes][8]    A[i=l%32][k=8(l/32)+e] = W1[32m+i][16s+k]
-//   hidden       [n_hidden][KS][NMB][64][8] columns permuted to the LDS chunk order
-//   output       [H/32][64][8]              A[i=l%16][k=8(l/16)+e] (16x16x32 layout)
-// followed by fp32 biases in C-fragment order.
+//   W1 fragments [ks1][NMB][64 lanes][8]      A[i=l%32][k=8(l/32)+e] = W1[32m+i][16s+k];
+//                                             columns F..F+2 hold the bias terms
+//   hidden       [n_hidden][KS+1][NMB][64][8] columns permuted to the LDS chunk
+//                                             order; K-step KS holds the bias terms
+//   output       [H/32][64][8]                A[i=l%16][k=8(l/16)+e] (16x16x32 layout)
 size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
-                 std::vector<uint16_t> &frags, std::vector<float> &bias1, std::vector<float> &biash,
-                 BF16Packed *pk) {
+                 std::vector<uint16_t> &frags, BF16Packed *pk) {
     const int H = dims[1], Fin = dims[0], Fout = dims[n_layers];
-    const int NMB = H / 32, KS = H / 16, ks1 = (Fin + 15) / 16;
+    const int NMB = H / 32, KS = H / 16, ks1 = (Fin + 3 + 15) / 16;
     const int n_hidden = n_layers - 2;
     frags.clear();
     pk->off_w1 = 0;
@@ -341,17 +390,33 @@ size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const
             for (int l = 0; l < 64; ++l)
                 for (int e = 0; e < 8; ++e) {
                     const int o = 32 * m + l % 32, k = 16 * s + 8 * (l / 32) + e;
-                    frags.push_back(k < Fin ? bf16_bits_host(W[0][(size_t)o * Fin + k]) : 0);
+                    uint16_t v = 0;
+                    if (k < Fin) {
+                        v = bf16_rne_host(W[0][(size_t)o * Fin + k]);
+                    } else if (k < Fin + 3) {
+                        uint16_t t[3];
+                        split_bias(b[0][o], t);
+                        v = t[k - Fin];
+                    }
+                    frags.push_back(v);
                 }
     pk->off_wh = (int64_t)(frags.size() / 8);
     for (int h = 0; h < n_hidden; ++h)
-        for (int s = 0; s < KS; ++s)
+        for (int s = 0; s <= KS; ++s)
             for (int m = 0; m < NMB; ++m)
                 for (int l = 0; l < 64; ++l)
                     for (int e = 0; e < 8; ++e) {
                         const int o = 32 * m + l % 32;
-                        const int k = chunk_feature(2 * s + l / 32, e);
-                        frags.push_back(bf16_bits_host(W[h + 1][(size_t)o * H + k]));
+                        uint16_t v = 0;
+                        if (s < KS) {
+                            const int k = chunk_feature(2 * s + l / 32, e);
+                            v = bf16_rne_host(W[h + 1][(size_t)o * H + k]);
+                        } else if (l / 32 == 0 && e < 3) {
+                            uint16_t t[3];
+                            split_bias(b[h + 1][o], t);
+                            v = t[e];
+                        }
+                        frags.push_back(v);
                     }
     pk->off_wo = (int64_t)(frags.size() / 8);
     for (int s = 0; s < H / 32; ++s)
@@ -359,21 +424,8 @@ size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const
             for (int e = 0; e < 8; ++e) {
                 const int i = l % 16;
                 const int k = chunk_feature(4 * s + l / 16, e);
-                frags.push_back(i < Fout ? bf16_bits_host(W[n_layers - 1][(size_t)i * H + k]) : 0);
+                frags.push_back(i < Fout ? bf16_rne_host(W[n_layers - 1][(size_t)i * H + k]) : 0);
             }
-    auto cbias = [&](const float *bb, std::vector<float> &dst) {
-        for (int m = 0; m < NMB; ++m)
-            for (int g = 0; g < 2; ++g)
-                for (int r = 0; r < 16; ++r)
-                    dst.push_back(bb[32 * m + 8 * (r / 4) + 4 * g + (r % 4)]);
-    };
-    bias1.clear();
-    biash.clear();
-    cbias(b[0], bias1);
-    for (int h = 0; h < n_hidden; ++h)
-        cbias(b[h + 1], biash);
-    if (biash.empty())
-        biash.push_back(0.f);
     pk->frag_bytes = (uint32_t)(frags.size() * 2);
     pk->hid = H;
     pk->n_hidden = n_hidden;
@@ -384,12 +436,12 @@ size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const
     return frags.size();
 }
 
-hipError_t launch_mlp_bf16(const DevMap &in, const DevMap &out, const BF16Packed &pk, hipStream_t stream) {
+hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const BF16Packed &pk, hipStream_t stream) {
     if (in.n_points == 0)
         return hipSuccess;
     if (pk.hid == 512)
         return pk.ks1 <= 1 ? launch_t<512, 1>(in, out, pk, stream) : launch_t<512, 4>(in, out, pk, stream);
-    return pk.ks1 <= 1 ? launch_t<256, 1>(in, out, pk, stream) : launch_t<256, 2>(in, out, pk, stream);
+    return launch_t<256, 1>(in, out, pk, stream);
 }
 
 const char *bf16_variant_name(const BF16Packed &pk) {

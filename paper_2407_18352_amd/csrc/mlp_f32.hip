@@ -84,8 +84,8 @@ __device__ __forceinline__ void load_bias(const float *bias, int g, floatx16 *ac
 }
 
 template <int NMB, int KS1MAX>
-__global__ void __launch_bounds__(512) mlp_f32_kernel(DevMap in, DevMap out, F32Packed pk,
-                                                      int64_t n_tiles) {
+__global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, F32Packed pk,
+                                                      int32_t n_tiles) {
     extern __shared__ float lds[];
     // stage the packed weights once per block
     {
@@ -97,6 +97,12 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(DevMap in, DevMap out, F32
     }
     __syncthreads();
 
+    __shared__ LdsPlan<64, 64> pin;     // F_in <= 64
+    __shared__ LdsPlan<8, 8> pout;      // F_out <= 8
+    pin.stage(in);
+    pout.stage(out);
+    __syncthreads();
+
     const F32Layout lay{NMB, pk.ks1, pk.n_hidden, pk.f_out};
     const int lane = threadIdx.x & 63;
     const int g = lane >> 5;
@@ -105,37 +111,35 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(DevMap in, DevMap out, F32
     // XCD-aware order: blocks of one XCD (hardware id % 8) take adjacent tiles
     const int nb = gridDim.x;
     const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
-    const int64_t wave_id = (int64_t)lb * waves_per_block + (threadIdx.x >> 6);
-    const int64_t n_waves = (int64_t)nb * waves_per_block;
+    const int wave_id = lb * waves_per_block + (threadIdx.x >> 6);
+    const int n_waves = nb * waves_per_block;
     const int F = in.n_features;
 
-    for (int64_t tile = wave_id; tile < n_tiles; tile += n_waves) {
-        const int64_t b = tile * 32 + col;
+    for (int tile = wave_id; tile < n_tiles; tile += n_waves) {
+        const int b = tile * 32 + col;
         const bool valid = b < in.n_points;
 
-        // ---- gather: lane (col, g) loads feature 2s+g of point b for K-step s
+        // ---- gather: lane (col, g) loads feature 2s+g of point b for K-step s.
+        //      Loads are unconditional (feature numbers clamped into the plan;
+        //      unused values zeroed afterwards) so no branch separates them;
+        //      a wave whose points all read inside the arrays skips boundary
+        //      resolution.
         float x[KS1MAX];
         {
-            int64_t p[HPACML_MAX_RANK];
-            sweep_point(in, valid ? b : 0, p);
-            const bool inside = interior(in, p);
-            const int64_t pe = point_elem(in, p, 0);
+            const Pt32 pt = locate32(in, valid ? b : in.n_points - 1);
+            const bool fast = __all(pt.inside);          // no boundary resolution anywhere
 #pragma unroll
             for (int s = 0; s < KS1MAX; ++s) {
-                x[s] = 0.f;
-                if (s < pk.ks1) {
-                    const int f = 2 * s + g;
-                    const int fc = f < F ? f : F - 1;
-                    const FeatureEntry e = in.feat[fc];
-                    int64_t idx;
-                    if (inside)
-                        idx = (in.same_strides ? pe : point_elem(in, p, e.target)) + e.delta;
-                    else
-                        idx = resolved_elem(in, p, e);
-                    if (valid && f < F)
-                        x[s] = in.base[e.target][idx];
-                }
+                const int f = 2 * s + g;
+                const FeatureEntry e = pin.feat[f < F ? f : F - 1];
+                const int32_t idx = fast ? pt.pe + (int32_t)e.delta : elem32(in, pt, e);
+                x[s] = ldg(pin.base[e.target] + idx);
+                if (s % 8 == 7)
+                    __builtin_amdgcn_sched_barrier(0);   // bound the live addresses
             }
+#pragma unroll
+            for (int s = 0; s < KS1MAX; ++s)
+                x[s] = (valid && 2 * s + g < F) ? x[s] : 0.f;
         }
 
         floatx16 acc[NMB];
@@ -184,10 +188,7 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(DevMap in, DevMap out, F32
         }
 
         // ---- output layer (VALU) + scatter through the `from` map
-        int64_t po[HPACML_MAX_RANK];
-        sweep_point(out, valid ? b : 0, po);
-        const bool oin = interior(out, po);
-        const int64_t ope = point_elem(out, po, 0);
+        const Pt32 po = locate32(out, valid ? b : in.n_points - 1);
         const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
         for (int go = 0; go < pk.f_out; ++go) {
             const float *w = lds + lay.out_w() + (go * 2 + g) * (16 * NMB);
@@ -207,18 +208,16 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(DevMap in, DevMap out, F32
             if (orelu)
                 y = fmaxf(y, 0.f);
             if (g == 0 && valid) {
-                const FeatureEntry e = out.feat[go];
-                int64_t idx = oin ? (out.same_strides ? ope : point_elem(out, po, e.target)) + e.delta
-                                  : resolved_elem(out, po, e);
-                out.base[e.target][idx] = y;
+                const FeatureEntry e = pout.feat[go];
+                stg(pout.base[e.target] + elem32(out, po, e), y);
             }
         }
     }
 }
 
 template <int NMB, int KS1MAX>
-hipError_t launch_t(const DevMap &in, const DevMap &out, const F32Packed &pk, hipStream_t stream) {
-    const int64_t n_tiles = (in.n_points + 31) / 32;
+hipError_t launch_t(const Map32 &in, const Map32 &out, const F32Packed &pk, hipStream_t stream) {
+    const int32_t n_tiles = (in.n_points + 31) / 32;
     const int threads = NMB == 4 ? 512 : 256;
     const int waves = threads / 64;
     const size_t lds = (size_t)pk.lds_bytes;
@@ -301,7 +300,7 @@ void f32_pack(int n_layers, const int32_t *dims, const float *const *W, const fl
         img[lay.out_b() + go] = b[n_layers - 1][go];
 }
 
-hipError_t launch_mlp_f32(const DevMap &in, const DevMap &out, const F32Packed &pk, hipStream_t stream) {
+hipError_t launch_mlp_f32(const Map32 &in, const Map32 &out, const F32Packed &pk, hipStream_t stream) {
     if (in.n_points == 0)
         return hipSuccess;
     if (pk.hid == 128)
