@@ -21,6 +21,8 @@ struct hpacml_map_s {
     DevMap dev{};
     Map32 m32{};
     bool fast = false;   // m32 is valid
+    bool c32 = false;    // the 32-bit collect kernel applies (cargs valid)
+    CollectArgs32 cargs{};
 };
 
 enum class Variant { Generic, F32, BF16 };
@@ -211,6 +213,7 @@ bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *ba
             if ((uint32_t)(((uint64_t)n * m.magic[d]) >> m.shift[d]) != n / (uint32_t)dv)
                 return false;
     }
+    m.raw8 = p.raw8 ? 1 : 0;
     m.feat = feat_dev;
     m.base = base_dev;
     *out = m;
@@ -298,6 +301,9 @@ hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir, const hpac
         }
         m->dev = make_devmap(m->plan, m->feat_dev, m->base_dev, m->stride_dev);
         m->fast = make_map32(m->plan, m->feat_dev, m->base_dev, &m->m32);
+        m->c32 = collect32_supported(m->plan, m->fast);
+        if (m->c32)
+            collect32_args(m->plan, &m->cargs);
         *out = m;
         return HPACML_OK;
     } catch (const std::bad_alloc &) {
@@ -488,7 +494,9 @@ hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *
         if (!((const char *)dst + need <= a0 || a1 <= (const char *)dst))
             return HPACML_E_ALIAS;
     }
-    return hip_status(launch_collect(m->dev, reinterpret_cast<uint32_t *>(dst), ld, (hipStream_t)stream));
+    uint32_t *d = reinterpret_cast<uint32_t *>(dst);
+    return hip_status(m->c32 ? launch_collect32(m->m32, m->cargs, d, ld, (hipStream_t)stream)
+                             : launch_collect(m->dev, d, ld, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -2,31 +2,49 @@
 // dense record dst[p * ld + f] (Sec. III-A-2 and Sec. IV-B: the region's
 // mapped inputs and outputs are stored for training).
 //
-// HBM-bound.  Each block owns tiles of WAVES x 64 sweep points.  Phase 1: one
-// lane per point walks the features (the feature index is wave-uniform, so
-// the plan entry comes through scalar loads) and loads with coalesced reads
-// along the sweep; values land in an LDS tile [point][feature].  Phase 2: the
-// block writes the tile's record rows as contiguous runs of F words.
+// HBM-bound: every point's F values are read once from the application
+// arrays and written once to the record.  One block per tile of P sweep
+// points (P = 64 x waves, sized so that several blocks share a CU and keep
+// enough loads and stores in flight).  Phase 1: one lane per point walks the
+// features in batches whose loads are all issued before the first use (the
+// feature index is wave-uniform and its plan entry comes from LDS); the
+// values land in an LDS tile laid out exactly as the record rows [point][F].
+// Phase 2: the tile's rows form one contiguous run of the record when
+// ld == F, which the block writes with 16-byte stores; otherwise row by row.
+#include <type_traits>
+
 #include "kernels.hpp"
 
 namespace hpacml {
 
 namespace {
 
-constexpr int kBatch = 8;
+constexpr int kBatch = 16;
 
-__global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__restrict__ dst,
-                                                      int64_t ld, int pitch, int64_t n_tiles) {
-    extern __shared__ uint32_t tile[];
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void stg4(uint32_t *p, u32x4 v) {
+    __builtin_nontemporal_store(v, (__attribute__((address_space(1))) u32x4 *)p);
+}
+__device__ __forceinline__ void stg1(uint32_t *p, uint32_t v) {
+    __builtin_nontemporal_store(v, (__attribute__((address_space(1))) uint32_t *)p);
+}
+
+// idx / F for idx < 2^16 and F <= 256: with M = ceil(2^24 / F) the error term
+// idx * (M * F - 2^24) stays below 2^24, so the quotient is exact.
+__device__ __forceinline__ uint32_t div_small(uint32_t idx, uint32_t magic) { return (idx * magic) >> 24; }
+
+template <bool DENSE>
+__global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__restrict__ dst, int64_t ld,
+                                                      uint32_t magic, int64_t n_tiles) {
+    extern __shared__ u32x4 tile4[];
+    uint32_t *tile = reinterpret_cast<uint32_t *>(tile4);
     __shared__ LdsPlan<HPACML_MAX_FEATURES, HPACML_MAX_TARGETS> plan;
     plan.stage(m);
     __syncthreads();
     const int F = m.n_features;
     const int P = blockDim.x;                  // points per tile (one per thread)
     const int t = threadIdx.x;
-    // phase-2 walk: linear element t of the tile is (row t / F, column t % F)
-    const int step_r = P / F, step_f = P % F;
-    const int r0 = t / F, f0 = t % F;
 
     for (int64_t tileno = blockIdx.x; tileno < n_tiles; tileno += gridDim.x) {
         const int64_t b0 = tileno * P;
@@ -36,63 +54,167 @@ __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__rest
         sweep_point(m, valid ? b : m.n_points - 1, p);
         const bool inside = interior(m, p);
         const int64_t pe = point_elem(m, p, 0);
+        const bool fast = __all(inside) && m.same_strides;   // no boundary resolution in this wave
 
-        // feature-uniform batches; loads unconditional (feature numbers
-        // clamped) so a batch has all its loads in flight at once
         for (int fb = 0; fb < F; fb += kBatch) {
             uint32_t v[kBatch];
+            if (fast) {
 #pragma unroll
-            for (int k = 0; k < kBatch; ++k) {
-                const int f = fb + k < F ? fb + k : F - 1;
-                const FeatureEntry e = plan.feat[f];
-                v[k] = ldg_bits(plan.base[e.target] + gather_elem(m, p, inside, pe, e));
+                for (int k = 0; k < kBatch; ++k) {
+                    const int f = fb + k < F ? fb + k : F - 1;
+                    const FeatureEntry e = plan.feat[f];
+                    v[k] = ldg_bits(plan.base[e.target] + pe + e.delta);
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < kBatch; ++k) {
+                    const int f = fb + k < F ? fb + k : F - 1;
+                    const FeatureEntry e = plan.feat[f];
+                    v[k] = ldg_bits(plan.base[e.target] + gather_elem(m, p, inside, pe, e));
+                }
             }
 #pragma unroll
             for (int k = 0; k < kBatch; ++k)
                 if (fb + k < F)
-                    tile[t * pitch + fb + k] = v[k];
+                    tile[t * F + fb + k] = v[k];
         }
         __syncthreads();
 
-        const int64_t rows = (m.n_points - b0) < P ? (m.n_points - b0) : P;
-        int r = r0, f = f0;
-        for (int64_t idx = t; idx < rows * F; idx += P) {
-            dst[(b0 + r) * ld + f] = tile[r * pitch + f];
-            r += step_r;
-            f += step_f;
-            if (f >= F) {
-                f -= F;
-                r += 1;
+        const int rows = (m.n_points - b0) < P ? (int)(m.n_points - b0) : P;
+        const int n = rows * F;                    // words of this tile
+        if (DENSE) {
+            // rows b0.. are one run starting at dst + b0 * F (16-byte aligned:
+            // dst is, and P * F is a multiple of 4)
+            uint32_t *run = dst + b0 * F;
+            for (int q = t; q < n / 4; q += P)
+                stg4(run + 4 * q, tile4[q]);
+            for (int i = (n & ~3) + t; i < n; i += P)
+                stg1(run + i, tile[i]);
+        } else {
+            for (int i = t; i < n; i += P) {
+                const uint32_t r = div_small((uint32_t)i, magic);
+                const uint32_t f = (uint32_t)i - r * (uint32_t)F;
+                stg1(dst + (b0 + r) * ld + f, tile[i]);
             }
         }
         __syncthreads();
     }
 }
 
+// 32-bit form: Map32 view, feature table in the kernel arguments, one tile
+// of 64 * WAVES points per block (no block loops over tiles), and boundary
+// resolution only along the dimensions where the wave touches an edge.
+template <bool DENSE, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, CollectArgs32 c, uint32_t *__restrict__ dst,
+                                                               int64_t ld, uint32_t magic, int32_t n_tiles) {
+    extern __shared__ u32x4 tile4[];
+    uint32_t *tile = reinterpret_cast<uint32_t *>(tile4);
+    constexpr int P = 64 * WAVES;
+    const int F = m.n_features;
+    const int t = threadIdx.x;
+    // XCD-aware order: the blocks of one XCD (blockIdx % 8) take one
+    // contiguous range of tiles, so neighbouring windows share its L2
+    const int32_t xq = n_tiles / 8, xr = n_tiles % 8, xx = blockIdx.x % 8;
+    const int32_t tileno = xx * xq + (xx < xr ? xx : xr) + blockIdx.x / 8;
+    const int32_t b0 = tileno * P;
+    const int32_t b = b0 + t;
+    const Pt32 pt = locate32(m, b < m.n_points ? b : m.n_points - 1);
+    const uint32_t edge = edge_dims32(m, pt);
+
+    // batches of K features: table entries fb..fb+K-1 exist (fb + K <= 64)
+    auto batch = [&](int fb, auto kb) {
+        constexpr int K = decltype(kb)::value;
+        uint32_t v[K];
+        if (edge == 0) {
+#pragma unroll
+            for (int k = 0; k < K; ++k)
+                v[k] = ldg_bits(c.fptr[fb + k] + pt.pe);
+        } else {
+#pragma unroll
+            for (int k = 0; k < K; ++k)
+                v[k] = ldg_bits(c.fptr[fb + k] + (pt.pe + edge_fix32(m, pt, c.raw8[fb + k], edge)));
+        }
+#pragma unroll
+        for (int k = 0; k < K; ++k)
+            if (fb + k < F)
+                tile[t * F + fb + k] = v[k];
+    };
+    int fb = 0;
+    for (; fb + 8 <= F; fb += 8)
+        batch(fb, std::integral_constant<int, 8>{});
+    for (; fb < F; fb += 4)
+        batch(fb, std::integral_constant<int, 4>{});
+    __syncthreads();
+
+    const int rows = (m.n_points - b0) < P ? (m.n_points - b0) : P;
+    const int n = rows * F;                        // words of this tile
+    if (DENSE) {
+        uint32_t *run = dst + (int64_t)b0 * F;     // 16-byte aligned: dst is, P * F is a multiple of 4
+        for (int q = t; q < n / 4; q += P)
+            stg4(run + 4 * q, tile4[q]);
+        for (int i = (n & ~3) + t; i < n; i += P)
+            stg1(run + i, tile[i]);
+    } else {
+        for (int i = t; i < n; i += P) {
+            const uint32_t r = div_small((uint32_t)i, magic);
+            const uint32_t f = (uint32_t)i - r * (uint32_t)F;
+            stg1(dst + ((int64_t)b0 + r) * ld + f, tile[i]);
+        }
+    }
+}
+
+template <bool DENSE, int WAVES>
+hipError_t launch_c32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
+    constexpr int P = 64 * WAVES;
+    const int F = m.n_features;
+    const int32_t n_tiles = (int32_t)(((int64_t)m.n_points + P - 1) / P);
+    const size_t lds = (size_t)P * F * sizeof(uint32_t);
+    const uint32_t magic = (uint32_t)(((1u << 24) + F - 1) / F);
+    hipLaunchKernelGGL((collect32_kernel<DENSE, WAVES>), dim3((unsigned)n_tiles), dim3(P), lds, stream, m, c, dst,
+                       ld, magic, n_tiles);
+    return hipGetLastError();
+}
+
 }  // namespace
+
+bool collect32_supported(const MapPlan &p, bool map32) {
+    return map32 && p.raw8 && p.n_features >= 1 && p.n_features <= kCollectMaxF;
+}
+
+void collect32_args(const MapPlan &p, CollectArgs32 *out) {
+    for (int f = 0; f < kCollectMaxF; ++f) {
+        const FeatureEntry &e = p.feat[f < p.n_features ? f : p.n_features - 1];
+        out->fptr[f] = (const float *)p.base[e.target] + e.delta;
+        out->raw8[f] = e.raw8;
+    }
+}
+
+hipError_t launch_collect32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
+    if (m.n_points == 0)
+        return hipSuccess;
+    const bool dense = ld == m.n_features && ((uintptr_t)dst & 15u) == 0;
+    return dense ? launch_c32<true, 1>(m, c, dst, ld, stream) : launch_c32<false, 1>(m, c, dst, ld, stream);
+}
 
 hipError_t launch_collect(const DevMap &m, uint32_t *dst, int64_t ld, hipStream_t stream) {
     if (m.n_points == 0)
         return hipSuccess;
-    const int pitch = m.n_features | 1;        // odd pitch: conflict-free phase-1 stores
-    // up to 4 waves, LDS tile at most 64 KB
-    int waves = 16384 / (64 * pitch);
+    const int F = m.n_features;
+    // tile of P = 64 x waves points, its LDS at most ~40 KB (four or more
+    // blocks per CU)
+    int waves = 40960 / (256 * F);
     waves = waves < 1 ? 1 : (waves > 4 ? 4 : waves);
     const int threads = 64 * waves;
-    const size_t lds = (size_t)threads * pitch * sizeof(uint32_t);
+    const size_t lds = (size_t)threads * F * sizeof(uint32_t);
     const int64_t n_tiles = (m.n_points + threads - 1) / threads;
-    // LDS per block bounds the blocks per CU; 256 CUs
-    int per_cu = (int)(65536 / lds);
-    per_cu = per_cu < 1 ? 1 : (per_cu > 8 ? 8 : per_cu);
-    int64_t grid = 256LL * per_cu;
-    if (grid > n_tiles)
-        grid = n_tiles;
-    hipError_t e = hipFuncSetAttribute((const void *)collect_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    const int64_t grid = n_tiles < 0x7FFFFFFF ? n_tiles : 0x7FFFFFFF;
+    const uint32_t magic = (uint32_t)(((1u << 24) + F - 1) / F);
+    const bool dense = ld == F && ((uintptr_t)dst & 15u) == 0;
+    auto kern = dense ? collect_kernel<true> : collect_kernel<false>;
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(collect_kernel, dim3((unsigned)grid), dim3(threads), lds, stream, m, dst, ld,
-                       pitch, n_tiles);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, stream, m, dst, ld, magic, n_tiles);
     return hipGetLastError();
 }
 

@@ -154,6 +154,7 @@ struct Map32 {
     int32_t bnd[HPACML_MAX_RANK], omin[HPACML_MAX_RANK], omax[HPACML_MAX_RANK];
     uint32_t magic[HPACML_MAX_RANK];
     int32_t shift[HPACML_MAX_RANK];
+    int32_t raw8;                      // FeatureEntry::raw8 is valid (elem32_edge applies)
     const FeatureEntry *feat;          // device
     float *const *base;                // device
 };
@@ -204,6 +205,40 @@ __device__ __forceinline__ int32_t elem32(const Map32 &m, const Pt32 &r, const F
         }
     }
     return r.inside ? r.pe + (int32_t)e.delta : res;
+}
+
+// Dimensions along which some lane of the wave reads outside the arrays:
+// bit d set when any lane's window leaves [0, extent) along d (wave-uniform).
+__device__ __forceinline__ uint32_t edge_dims32(const Map32 &m, const Pt32 &r) {
+    uint32_t edge = 0;
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d)
+        if (d < m.rank && __any(r.p[d] + m.omin[d] < 0 || r.p[d] + m.omax[d] >= m.extent[d]))
+            edge |= 1u << d;
+    return edge;
+}
+
+// Boundary correction of a feature with raw offsets `raw8` at point r, for
+// maps with Map32::raw8: the element index of the access is the interior
+// index (point + offset) plus this.  Only the dimensions in the wave-uniform
+// set `edge` are resolved (elsewhere every lane is inside and the correction
+// is zero): periodic wraps once (|offset| <= extent), clamp saturates.
+__device__ __forceinline__ int32_t edge_fix32(const Map32 &m, const Pt32 &r, uint32_t raw8, uint32_t edge) {
+    int32_t fix = 0;
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        if (edge & (1u << d)) {
+            const int32_t q = r.p[d] + (int32_t)(int8_t)(raw8 >> (8 * d));
+            const int32_t n = m.extent[d];
+            int32_t c;
+            if (m.bnd[d] == HPACML_BND_PERIODIC)
+                c = (n & (q >> 31)) - (n & ~((q - n) >> 31));   // +n below 0, -n at or past n
+            else
+                c = max(0, min(q, n - 1)) - q;
+            fix += c * m.stride[d];
+        }
+    }
+    return fix;
 }
 
 // Per-block LDS copy of the parts of a plan that the gathers index with a

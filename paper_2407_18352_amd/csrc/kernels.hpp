@@ -26,6 +26,19 @@ struct DevModel {
 // Collect: dst[p * ld + f] = bits of feature f at point p.
 hipError_t launch_collect(const DevMap &m, uint32_t *dst, int64_t ld, hipStream_t stream);
 
+// Feature table of a map passed by value to the 32-bit collect kernel (kernel
+// arguments are read through the scalar cache): maps with a Map32 view,
+// Map32::raw8 and at most 64 features.  Entries past the last feature repeat
+// it, so a batch of eight may read the table unconditionally.
+constexpr int kCollectMaxF = 64;
+struct CollectArgs32 {
+    const float *fptr[kCollectMaxF];  // target base + interior offset of feature f
+    uint32_t raw8[kCollectMaxF];      // raw offsets, signed bytes
+};
+bool collect32_supported(const MapPlan &p, bool map32);
+void collect32_args(const MapPlan &p, CollectArgs32 *out);
+hipError_t launch_collect32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int64_t ld, hipStream_t stream);
+
 // General-shape fused gather -> MLP -> scatter (VALU, any widths).
 hipError_t launch_mlp_generic(const DevMap &in, const DevMap &out, const DevModel &mdl,
                               hipStream_t stream);

@@ -72,6 +72,23 @@ __device__ __forceinline__ uint4 pack8(const float *v) {
     return q;
 }
 
+// ReLU on a packed bf16 pair, with max(x, 0) = 0 for a NaN x as in fp32.
+// As 16-bit integers the values kept are exactly 0x0000..0x7F80 (+0 up to
+// +Inf); every other pattern (negative, -0, NaN of either sign) becomes +0:
+// adding 0x7F sends the positive NaNs past 0x7FFF (negative as int16) and
+// the negative NaNs to 0..0x7E, all of which a signed max with 0x7F then
+// floors.  Rounding and ReLU commute, so this equals rounding max(x, 0).
+typedef short shortx2 __attribute__((ext_vector_type(2)));
+typedef unsigned short ushortx2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t relu2(uint32_t v) {
+    const ushortx2 k = {0x7F, 0x7F};
+    const ushortx2 u = __builtin_bit_cast(ushortx2, v) + k;
+    const shortx2 m = __builtin_elementwise_max(__builtin_bit_cast(shortx2, u), __builtin_bit_cast(shortx2, k));
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(ushortx2, m) - k);
+}
+
+__device__ __forceinline__ uint4 relu8(uint4 q) { return uint4{relu2(q.x), relu2(q.y), relu2(q.z), relu2(q.w)}; }
+
 // feature held at element e of LDS chunk c (C layout of the 32x32 MFMA,
 // two chunks per (m-block, lane half))
 __host__ __device__ inline int chunk_feature(int c, int e) {
@@ -98,9 +115,11 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                                                             int32_t n_tiles) {
     using G = Geo<H>;
     constexpr int PX = 2 * KS1MAX + 1;             // gathered-input row pitch (chunks)
+    constexpr int KO = H / 32;                     // output-layer K-steps
     extern __shared__ uint4 smem[];
     uint4 *Hs = smem;                              // [T][PH] activations
-    uint4 *Xs = smem + G::T * G::PH;               // [T][PX] gathered inputs
+    uint4 *Xs = smem + G::T * G::PH;               // [T][PX] gathered inputs, then
+    uint4 *Wo = Xs;                                //   [KO][64] output-layer fragments
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = tid >> 6;
@@ -130,8 +149,45 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
     const int nb = gridDim.x;
     const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
 
+    // scatter through the `from` map: lane (l%16 = point, l/16 = output
+    // group) of wave w holds outputs 4(l/16)..+3 of point w*T/8 + 16n + l%16
+    floatx4 y_prev[G::NB16];
+    int b0_prev = -1;
+    const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
+    auto scatter = [&](int bs) {
+        const int q = lane >> 4, pc = lane & 15;
+#pragma unroll
+        for (int n = 0; n < G::NB16; ++n) {
+            const int b = bs + w * (G::T / 8) + 16 * n + pc;
+            const Pt32 pt = locate32(out, b < out.n_points ? b : out.n_points - 1);
+            const bool fast = __all(pt.inside);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int go = 4 * q + r;
+                if (go < pk.f_out && b < out.n_points) {
+                    float v = y_prev[n][r] + pk.bias_out[go];
+                    if (orelu)
+                        v = fmaxf(v, 0.f);
+                    const FeatureEntry fe = pout.feat[go];
+                    const int32_t idx = fast ? pt.pe + (int32_t)fe.delta : elem32(out, pt, fe);
+                    stg(pout.base[fe.target] + idx, v);
+                }
+            }
+        }
+    };
+
     for (int tile = lb; tile < n_tiles; tile += nb) {
         const int b0 = tile * G::T;
+
+        // first-layer weight fragments, fetched before the gather so they
+        // arrive while the gather's loads are in flight
+        uint4 a1[KS1MAX][2];
+#pragma unroll
+        for (int s = 0; s < KS1MAX; ++s)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                a1[s][j] = s < pk.ks1 ? wload(wr, vlane + j * 1024, (uint32_t)((pk.off_w1 + (int64_t)s * G::NMB * 64) * 16))
+                                      : uint4{0u, 0u, 0u, 0u};
 
         // ---- gather: (point, chunk) pairs, 8 features per chunk, rounded to
         //      bf16; features F..F+2 are the constant 1 that carries the
@@ -161,6 +217,9 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                     v[it][e] = ldg(pin.base[fe.target] + idx);
                 }
             }
+            if (b0_prev >= 0)
+                scatter(b0_prev);                        // previous tile's outputs
+            __syncthreads();                             // previous tile's output layer is done with Wo
 #pragma unroll
             for (int it = 0; it < PASSES; ++it) {
                 const int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
@@ -183,25 +242,54 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
 #pragma unroll
         for (int s = 0; s < KS1MAX; ++s) {
             if (s < pk.ks1) {
-                uint4 a[2];
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    a[j] = wload(wr, vlane + j * 1024, (uint32_t)((pk.off_w1 + (int64_t)s * G::NMB * 64) * 16));
 #pragma unroll
                 for (int n = 0; n < 4; ++n) {
                     const bf16x8 bv = as_bf16x8(Xs[(p0 + 32 * n) * PX + 2 * s + g]);
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
                         acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            as_bf16x8(a[j]), bv, s == 0 ? floatx16{} : acc[j][n], 0, 0, 0);
+                            as_bf16x8(a1[s][j]), bv, s == 0 ? floatx16{} : acc[j][n], 0, 0, 0);
                 }
             }
         }
 
         // ---- hidden layers: epilogue of the previous layer (activation,
-        //      bf16 into LDS), then H x H plus the bias K-step
+        //      bf16 into LDS), then H x H plus the bias K-step.  The first
+        //      weight fragments of what follows (the next hidden layer, or the
+        //      output layer) are requested before the epilogue so their L2
+        //      latency hides behind it.
+        constexpr int KT = G::KS + 1;
+        constexpr int WO_PER_THREAD = (KO * 64 + kThreads - 1) / kThreads;
+        // output-layer fragments for this tile, requested now and stored to
+        // LDS (over the gathered inputs, dead after the first layer) once
+        // every wave is past the first layer
+        uint4 wo_stage[WO_PER_THREAD];
+#pragma unroll
+        for (int i = 0; i < WO_PER_THREAD; ++i) {
+            const int k = tid + i * kThreads;
+            wo_stage[i] = k < KO * 64 ? wload(wr, (uint32_t)(k * 16), (uint32_t)(pk.off_wo * 16)) : uint4{0u, 0u, 0u, 0u};
+        }
+        uint4 A[4][2];
         for (int h = 0; h <= pk.n_hidden; ++h) {
-            __syncthreads();               // every wave is done reading Hs
+            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * KT * G::NMB * 64) * 16);
+            auto load_a = [&](uint4 *dst, int s) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    dst[j] = wload(wr, vlane + j * 1024, wbase + (uint32_t)s * G::NMB * 1024);
+            };
+            if (h < pk.n_hidden) {
+                load_a(A[0], 0);
+                load_a(A[1], 1);
+            }
+            __syncthreads();               // every wave is done reading Hs (and Xs)
+            if (h == 0) {
+#pragma unroll
+                for (int i = 0; i < WO_PER_THREAD; ++i) {
+                    const int k = tid + i * kThreads;
+                    if (k < KO * 64)
+                        Wo[k] = wo_stage[i];
+                }
+            }
             if (pk.act[h] == HPACML_ACT_RELU) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
@@ -212,8 +300,8 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                             float v[8];
 #pragma unroll
                             for (int e = 0; e < 8; ++e)
-                                v[e] = fmaxf(acc[j][n][8 * sp + e], 0.f);
-                            Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = pack8(v);
+                                v[e] = acc[j][n][8 * sp + e];
+                            Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = relu8(pack8(v));
                         }
             } else {
 #pragma unroll
@@ -236,22 +324,12 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             // K loop, fully unrolled; scheduling barriers pin the pipeline:
             // weight fragments two K-steps ahead (ring of 4), activation
             // fragments one K-step ahead (ring of 2)
-            constexpr int KT = G::KS + 1;
-            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * KT * G::NMB * 64) * 16);
-            uint4 A[4][2];
             uint4 Bq[2][4];
-            auto load_a = [&](uint4 *dst, int s) {
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    dst[j] = wload(wr, vlane + j * 1024, wbase + (uint32_t)s * G::NMB * 1024);
-            };
             auto load_b = [&](uint4 *dst, int s) {
 #pragma unroll
                 for (int n = 0; n < 4; ++n)
                     dst[n] = Hs[(p0 + 32 * n) * G::PH + 2 * s + g];
             };
-            load_a(A[0], 0);
-            load_a(A[1], 1);
             load_b(Bq[0], 0);
 #pragma unroll
             for (int s = 0; s < KT; ++s) {
@@ -278,45 +356,35 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             const int q = lane >> 4, pc = lane & 15;
             floatx4 y[G::NB16];
 #pragma unroll
-            for (int s = 0; s < H / 32; ++s) {
-                const uint4 a = wload(wr, (uint32_t)(lane * 16), (uint32_t)((pk.off_wo + (int64_t)s * 64) * 16));
+            for (int s = 0; s < KO; ++s) {
+                const bf16x8 av = as_bf16x8(Wo[s * 64 + lane]);
 #pragma unroll
                 for (int n = 0; n < G::NB16; ++n) {
                     const int p = w * (G::T / 8) + 16 * n + pc;
                     const bf16x8 bv = as_bf16x8(Hs[p * G::PH + 4 * s + q]);
-                    y[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), bv, s == 0 ? floatx4{} : y[n],
-                                                                    0, 0, 0);
+                    y[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, s == 0 ? floatx4{} : y[n], 0, 0, 0);
                 }
             }
-            const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
+            // outputs stay in registers; they are scattered after the next
+            // tile's gather loads are issued (or after the loop)
 #pragma unroll
-            for (int n = 0; n < G::NB16; ++n) {
-                const int p = w * (G::T / 8) + 16 * n + pc;
-                const int b = b0 + p;
-                const Pt32 pt = locate32(out, b < out.n_points ? b : out.n_points - 1);
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int go = 4 * q + r;
-                    if (go < pk.f_out && b < out.n_points) {
-                        float v = y[n][r] + pk.bias_out[go];
-                        if (orelu)
-                            v = fmaxf(v, 0.f);
-                        const FeatureEntry fe = pout.feat[go];
-                        stg(pout.base[fe.target] + elem32(out, pt, fe), v);
-                    }
-                }
-            }
+            for (int n = 0; n < G::NB16; ++n)
+                y_prev[n] = y[n];
+            b0_prev = b0;
         }
-        // the next tile's gather writes Xs only: no wave reads Xs past the
-        // first layer, and Hs is not written again before a barrier
+        // the next tile's gather stores to Xs after a barrier; Hs is not
+        // written again before a barrier
     }
+    if (b0_prev >= 0)
+        scatter(b0_prev);
 }
 
 template <int H, int KS1MAX>
 hipError_t launch_t(const Map32 &in, const Map32 &out, const BF16Packed &pk, hipStream_t stream) {
     using G = Geo<H>;
     const int32_t n_tiles = (in.n_points + G::T - 1) / G::T;
-    const size_t lds = (size_t)G::T * (G::PH + 2 * KS1MAX + 1) * 16;
+    const size_t xs = (size_t)G::T * (2 * KS1MAX + 1) * 16, wo = (size_t)(H / 32) * 64 * 16;
+    const size_t lds = (size_t)G::T * G::PH * 16 + (xs > wo ? xs : wo);
     const int32_t grid = n_tiles < 256 ? n_tiles : 256;
     auto kern = mlp_bf16_kernel<H, KS1MAX>;
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -440,7 +508,8 @@ hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const BF16Packed &
     if (in.n_points == 0)
         return hipSuccess;
     if (pk.hid == 512)
-        return pk.ks1 <= 1 ? launch_t<512, 1>(in, out, pk, stream) : launch_t<512, 4>(in, out, pk, stream);
+        return pk.ks1 <= 1 ? launch_t<512, 1>(in, out, pk, stream)
+                           : (pk.ks1 <= 3 ? launch_t<512, 3>(in, out, pk, stream) : launch_t<512, 4>(in, out, pk, stream));
     return launch_t<256, 1>(in, out, pk, stream);
 }
 

@@ -190,16 +190,21 @@ hpacml_status build_map_plan(const hpacml_functor *f, int32_t dir, const hpacml_
 
     // per-feature table for the kernels
     p.feat.resize(p.n_features);
+    p.raw8 = true;
     {
         int fi = 0;
         for (int t = 0; t < n_targets; ++t)
             for (int k = 0; k < p.n_features / n_targets; ++k, ++fi) {
                 FeatureEntry &e = p.feat[fi];
                 e.target = t;
-                e.pad = 0;
+                e.raw8 = 0;
                 int64_t delta = 0;
                 for (int d = 0; d < HPACML_MAX_RANK; ++d) {
                     int64_t o = d < R ? p.raw[(size_t)fi * 4 + d] : 0;
+                    if (o < -127 || o > 127 || (p.bnd[d] == HPACML_BND_PERIODIC && (o > p.extent[d] || -o > p.extent[d])))
+                        p.raw8 = false;
+                    else
+                        e.raw8 |= (uint32_t)(uint8_t)(int8_t)o << (8 * d);
                     if (d < R && p.bnd[d] == HPACML_BND_PERIODIC)
                         e.off[d] = (int32_t)pos_mod(o, p.extent[d]);
                     else

@@ -22,7 +22,8 @@ struct FeatureEntry {
     int32_t target;     // which target array
     int32_t off[HPACML_MAX_RANK];  // offset from the sweep point, per dimension;
                                    // periodic dims: reduced into [0, extent)
-    int32_t pad;
+    uint32_t raw8;      // raw offsets as four signed bytes (dimension d in
+                        // bits 8d..8d+7); meaningful when MapPlan::raw8
     int64_t delta;      // element offset of an interior access:
                         // sum_d raw_offset[d] * stride[target][d]
 };
@@ -40,6 +41,9 @@ struct MapPlan {
     int32_t omax[HPACML_MAX_RANK] = {0, 0, 0, 0};
     bool pointwise = false;   // every feature reads the sweep point itself
     bool idx32 = false;       // every element index of every target fits in int32
+    bool raw8 = false;        // every raw offset fits a signed byte and, along a
+                              // periodic dimension, is at most the extent in size
+                              // (one wrap resolves it)
     std::vector<void *> base;             // [n_targets]
     std::vector<int64_t> stride;          // [n_targets * 4]
     std::vector<FeatureEntry> feat;       // [n_features]

@@ -65,6 +65,31 @@ def test_collect_preserves_bit_patterns_and_gaps():
     assert np.all(got[:, 9:] == 0xFFFFFFFF)          # columns >= F untouched
 
 
+@pytest.mark.parametrize("shape", [(33, 70), (5, 7), (61, 133)])
+def test_collect_dense_and_offset_records(shape):
+    """ld == F with a 16-byte aligned record (one contiguous run per tile,
+    vector stores) and the same record shifted by one word (row-wise path);
+    point counts that leave a ragged last tile and a word count that is not a
+    multiple of 4."""
+    import torch
+    g = np.random.default_rng(sum(shape))
+    a = g.standard_normal(shape).astype(np.float32)
+    spec = wl.window2d_spec(*shape)
+    want = oracle.collect(spec, [a])
+    dev = to_dev([a])
+    m = api.Map(spec, dev, _abi.TO)
+    F, n = m.n_features, m.n_points
+    rec = torch.empty(n * F + 8, device="cuda", dtype=torch.int32)
+    for off in (0, 1):
+        rec.fill_(-1)
+        api.collect(m, rec[off:].view(torch.float32), F)
+        torch.cuda.synchronize()
+        got = rec.cpu().numpy().view(np.uint32)
+        assert np.array_equal(got[off:off + n * F].reshape(n, F), want), off
+        assert np.all(got[:off] == 0xFFFFFFFF) and np.all(got[off + n * F:] == 0xFFFFFFFF), off
+    m.close()
+
+
 @pytest.mark.parametrize("R", [1, 2, 3])
 def test_collect_random_maps_bitexact(R):
     """Random functors, boundary modes, steps, sub-ranges and strided views."""
@@ -113,6 +138,29 @@ def test_infer_small(name):
     expY = np.stack([a.reshape(-1) for a in exp], 1)
     worst, norm = assert_close(gotY, expY, RTOL[w.compute], "%s via %s" % (name, var))
     print("%s [%s]: worst %.3e normwise %.3e" % (name, var, worst, norm))
+
+
+@pytest.mark.parametrize("name", wl.NAMES)
+def test_infer_nan_inputs_follow_relu(name):
+    """NaN inputs of either sign make the first layer NaN at the points that
+    read them; ReLU takes NaN to 0 (max(x, 0) = 0 unless x > 0), so every
+    output stays finite and matches the oracle under the usual bar."""
+    w = wl.make(name, "small")
+    g = np.random.default_rng(404)
+    for k, a in enumerate(w.inputs):
+        bits = a.reshape(-1).view(np.uint32)
+        at = g.choice(bits.size, size=6, replace=False)
+        bits[at[:3]] = 0x7FC00000
+        bits[at[3:5]] = 0xFFC00001
+        bits[at[5]] = 0x80000000                      # -0 stays a plain zero
+    got, var = run_infer(w)
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    assert not np.isnan(Y).any()
+    exp = [o.copy() for o in w.outputs]
+    oracle.scatter(w.out_spec, exp, Y)
+    gotY = np.stack([a.reshape(-1) for a in got], 1)
+    expY = np.stack([a.reshape(-1) for a in exp], 1)
+    assert_close(gotY, expY, RTOL[w.compute], "%s via %s" % (name, var))
 
 
 def test_infer_fast_paths_are_used():
