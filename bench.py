@@ -43,15 +43,16 @@ DESCRIPTION = {
 
 
 KERNEL_SOURCES = {
+    "collect": ["collect.hip", "device.hpp", "kernels.hpp"],
     "mlp_f32": ["mlp_f32.hip", "device.hpp", "kernels.hpp"],
     "mlp_bf16": ["mlp_bf16.hip", "device.hpp", "kernels.hpp"],
     "mlp_generic": ["mlp_generic.hip", "device.hpp", "kernels.hpp"],
 }
 
 
-def recorded_traffic(variant):
-    """HBM bytes per launch of `variant` from profiles/*.txt, if the kernel
-    source is unchanged since the counters were taken."""
+def recorded_traffic(variant, workload):
+    """HBM bytes per launch of `variant` on `workload` from profiles/*.txt,
+    if the kernel source is unchanged since the counters were taken."""
     fam = next((k for k in KERNEL_SOURCES if variant.startswith(k)), None)
     if fam is None:
         return None
@@ -64,9 +65,9 @@ def recorded_traffic(variant):
     sha = h.hexdigest()[:16]
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.txt"))):
         for line in open(path):
-            if line.startswith("traffic_line ") and ("kernel=%s " % variant) in line:
+            if line.startswith("traffic_line "):
                 kv = dict(t.split("=", 1) for t in line.split()[1:])
-                if kv.get("source_sha256") == sha:
+                if kv.get("kernel") == variant and kv.get("workload") == workload and kv.get("source_sha256") == sha:
                     return {"bytes": int(kv["bytes"]), "fetch": int(kv["fetch"]), "write": int(kv["write"]),
                             "source": os.path.relpath(path, ROOT)}
     return None
@@ -124,6 +125,8 @@ def main():
             ev[1].record(stream)
         api.collect(mi, rec_in, Fi, stream)
         api.collect(mo_rec, rec_out, Fo, stream)
+        if ev is not None:
+            ev[2].record(stream)
 
     if args.copy_calibration_mb:
         src = torch.empty(args.copy_calibration_mb << 18, device="cuda")
@@ -136,7 +139,7 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    evs = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3)) for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
@@ -147,14 +150,20 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = start.elapsed_time(stop)
-    infer_ms = [a.elapsed_time(b) for a, b in evs]
+    infer_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    collect_ms = [e[1].elapsed_time(e[2]) for e in evs]
     ms_step = total_ms / args.steps
     infer_avg = float(np.mean(infer_ms))
 
     flops_pt = w.flops_per_point
     achieved = flops_pt * B / (infer_avg * 1e-3)
     peak = PEAK[w.compute]
-    traffic = recorded_traffic(variant)
+    traffic = recorded_traffic(variant, args.workload)
+    # collect: every element of the mapped arrays read once, every record
+    # word written once (in and out records)
+    collect_bytes = (sum(a.nbytes for a in w.inputs) + 4 * B * Fi) + (sum(a.nbytes for a in w.outputs) + 4 * B * Fo)
+    collect_avg = float(np.mean(collect_ms))
+    collect_traffic = recorded_traffic("collect", args.workload)
     result = {
         "metric": "surrogate points/sec (gather+MLP+scatter) and % of HBM / MFMA roofline",
         "value": B / (ms_step * 1e-3),
@@ -178,7 +187,13 @@ def main():
                      "algorithmic_flop_per_launch": flops_pt * B},
         "infer_points_per_s": B / (infer_avg * 1e-3),
         "infer_ms": {"mean": infer_avg, "median": float(np.median(infer_ms)), "min": float(np.min(infer_ms))},
-        "collect_ms_per_step": ms_step - infer_avg,
+        "collect_roofline": {"bound": "hbm", "achieved": collect_bytes / (collect_avg * 1e-3) / 1e9,
+                             "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                             "frac": collect_bytes / (collect_avg * 1e-3) / HBM_PEAK,
+                             "traffic": collect_traffic["bytes"] if collect_traffic else None,
+                             "traffic_source": collect_traffic["source"] if collect_traffic else None,
+                             "algorithmic_bytes_per_step": collect_bytes, "ms_per_step": collect_avg,
+                             "kernels": "hpacml_collect of the input map and of the output map"},
         "wall_s_timed": wall,
     }
 

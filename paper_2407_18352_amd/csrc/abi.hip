@@ -21,8 +21,8 @@ struct hpacml_map_s {
     DevMap dev{};
     Map32 m32{};
     bool fast = false;   // m32 is valid
-    bool c32 = false;    // the 32-bit collect kernel applies (cargs valid)
-    CollectArgs32 cargs{};
+    bool t32 = false;    // tab is valid: 32-bit view, raw8, at most 64 features
+    FeatTable32 tab{};
 };
 
 enum class Variant { Generic, F32, BF16 };
@@ -220,6 +220,18 @@ bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *ba
     return true;
 }
 
+bool table32_supported(const MapPlan &p, bool map32) {
+    return map32 && p.raw8 && p.n_features >= 1 && p.n_features <= kTableMaxF;
+}
+
+void table32_make(const MapPlan &p, FeatTable32 *out) {
+    for (int f = 0; f < kTableMaxF; ++f) {
+        const FeatureEntry &e = p.feat[f < p.n_features ? f : p.n_features - 1];
+        out->fptr[f] = (const float *)p.base[e.target] + e.delta;
+        out->raw8[f] = e.raw8;
+    }
+}
+
 }  // namespace hpacml
 
 extern "C" {
@@ -301,9 +313,9 @@ hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir, const hpac
         }
         m->dev = make_devmap(m->plan, m->feat_dev, m->base_dev, m->stride_dev);
         m->fast = make_map32(m->plan, m->feat_dev, m->base_dev, &m->m32);
-        m->c32 = collect32_supported(m->plan, m->fast);
-        if (m->c32)
-            collect32_args(m->plan, &m->cargs);
+        m->t32 = table32_supported(m->plan, m->fast);
+        if (m->t32)
+            table32_make(m->plan, &m->tab);
         *out = m;
         return HPACML_OK;
     } catch (const std::bad_alloc &) {
@@ -442,7 +454,7 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
 const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
     if (check_infer(model, in, out) != HPACML_OK)
         return nullptr;
-    const bool fast = in->fast && out->fast;
+    const bool fast = in->t32 && out->t32;
     switch (fast ? model->variant : Variant::Generic) {
     case Variant::F32: return f32_variant_name(model->f32);
     case Variant::BF16: return bf16_variant_name(model->bf16);
@@ -459,10 +471,10 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
         return HPACML_OK;
     hipStream_t st = (hipStream_t)stream;
     hipError_t e;
-    const bool fast = in->fast && out->fast;
+    const bool fast = in->t32 && out->t32;
     switch (fast ? model->variant : Variant::Generic) {
-    case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, model->f32, st); break;
-    case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, model->bf16, st); break;
+    case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, in->tab, out->tab, model->f32, st); break;
+    case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, in->tab, out->tab, model->bf16, st); break;
     default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
     }
     return hip_status(e);
@@ -495,7 +507,7 @@ hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *
             return HPACML_E_ALIAS;
     }
     uint32_t *d = reinterpret_cast<uint32_t *>(dst);
-    return hip_status(m->c32 ? launch_collect32(m->m32, m->cargs, d, ld, (hipStream_t)stream)
+    return hip_status(m->t32 ? launch_collect32(m->m32, m->tab, d, ld, (hipStream_t)stream)
                              : launch_collect(m->dev, d, ld, (hipStream_t)stream));
 }
 

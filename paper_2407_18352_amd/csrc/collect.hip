@@ -105,7 +105,7 @@ __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__rest
 // of 64 * WAVES points per block (no block loops over tiles), and boundary
 // resolution only along the dimensions where the wave touches an edge.
 template <bool DENSE, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, CollectArgs32 c, uint32_t *__restrict__ dst,
+__global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTable32 c, uint32_t *__restrict__ dst,
                                                                int64_t ld, uint32_t magic, int32_t n_tiles) {
     extern __shared__ u32x4 tile4[];
     uint32_t *tile = reinterpret_cast<uint32_t *>(tile4);
@@ -164,7 +164,7 @@ __global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, CollectA
 }
 
 template <bool DENSE, int WAVES>
-hipError_t launch_c32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
+hipError_t launch_c32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
     constexpr int P = 64 * WAVES;
     const int F = m.n_features;
     const int32_t n_tiles = (int32_t)(((int64_t)m.n_points + P - 1) / P);
@@ -177,19 +177,7 @@ hipError_t launch_c32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int
 
 }  // namespace
 
-bool collect32_supported(const MapPlan &p, bool map32) {
-    return map32 && p.raw8 && p.n_features >= 1 && p.n_features <= kCollectMaxF;
-}
-
-void collect32_args(const MapPlan &p, CollectArgs32 *out) {
-    for (int f = 0; f < kCollectMaxF; ++f) {
-        const FeatureEntry &e = p.feat[f < p.n_features ? f : p.n_features - 1];
-        out->fptr[f] = (const float *)p.base[e.target] + e.delta;
-        out->raw8[f] = e.raw8;
-    }
-}
-
-hipError_t launch_collect32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
+hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
     if (m.n_points == 0)
         return hipSuccess;
     const bool dense = ld == m.n_features && ((uintptr_t)dst & 15u) == 0;

@@ -26,18 +26,19 @@ struct DevModel {
 // Collect: dst[p * ld + f] = bits of feature f at point p.
 hipError_t launch_collect(const DevMap &m, uint32_t *dst, int64_t ld, hipStream_t stream);
 
-// Feature table of a map passed by value to the 32-bit collect kernel (kernel
-// arguments are read through the scalar cache): maps with a Map32 view,
-// Map32::raw8 and at most 64 features.  Entries past the last feature repeat
-// it, so a batch of eight may read the table unconditionally.
-constexpr int kCollectMaxF = 64;
-struct CollectArgs32 {
-    const float *fptr[kCollectMaxF];  // target base + interior offset of feature f
-    uint32_t raw8[kCollectMaxF];      // raw offsets, signed bytes
+// Feature table of a map, passed by value to the 32-bit kernels (kernel
+// arguments are read through the scalar cache, so a wave-uniform feature
+// number costs no vector instruction): maps with a Map32 view, Map32::raw8
+// and at most 64 features.  Entries past the last feature repeat it, so
+// batches may read the table unconditionally.
+constexpr int kTableMaxF = 64;
+struct FeatTable32 {
+    const float *fptr[kTableMaxF];  // target base + interior offset of feature f
+    uint32_t raw8[kTableMaxF];      // raw offsets, signed bytes
 };
-bool collect32_supported(const MapPlan &p, bool map32);
-void collect32_args(const MapPlan &p, CollectArgs32 *out);
-hipError_t launch_collect32(const Map32 &m, const CollectArgs32 &c, uint32_t *dst, int64_t ld, hipStream_t stream);
+bool table32_supported(const MapPlan &p, bool map32);
+void table32_make(const MapPlan &p, FeatTable32 *out);
+hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream);
 
 // General-shape fused gather -> MLP -> scatter (VALU, any widths).
 hipError_t launch_mlp_generic(const DevMap &in, const DevMap &out, const DevModel &mdl,
@@ -58,8 +59,8 @@ bool f32_fast_supported(int n_layers, const int32_t *dims, int compute);
 size_t f32_image_floats(int n_layers, const int32_t *dims);
 void f32_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
               float *image);
-hipError_t launch_mlp_f32(const Map32 &in, const Map32 &out, const F32Packed &pk,
-                          hipStream_t stream);
+hipError_t launch_mlp_f32(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                          const F32Packed &pk, hipStream_t stream);
 const char *f32_variant_name(const F32Packed &pk);
 
 // bf16 fused kernel: hidden layers of one width H in {256, 512}; activations
@@ -78,8 +79,8 @@ struct BF16Packed {
 bool bf16_fast_supported(int n_layers, const int32_t *dims, int compute);
 size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
                  std::vector<uint16_t> &frags, BF16Packed *pk);
-hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const BF16Packed &pk,
-                           hipStream_t stream);
+hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                           const BF16Packed &pk, hipStream_t stream);
 const char *bf16_variant_name(const BF16Packed &pk);
 
 }  // namespace hpacml

@@ -111,7 +111,7 @@ struct Geo {
 };
 
 template <int H, int KS1MAX>
-__global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out, BF16Packed pk,
+__global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16Packed pk,
                                                             int32_t n_tiles) {
     using G = Geo<H>;
     constexpr int PX = 2 * KS1MAX + 1;             // gathered-input row pitch (chunks)
@@ -133,10 +133,12 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
     const __amdgpu_buffer_rsrc_t wr = weight_rsrc(pk.frags, pk.frag_bytes);
     const uint32_t vlane = (uint32_t)((m0 * 64 + lane) * 16);
 
-    __shared__ LdsPlan<64, 64> pin;                // F_in <= 64 features
-    __shared__ LdsPlan<16, 16> pout;               // F_out <= 16
-    pin.stage(in);
-    pout.stage(out);
+    __shared__ const float *so_ptr[16];             // output table, F_out <= 16
+    __shared__ uint32_t so_raw[16];
+    if (tid < 16) {
+        so_ptr[tid] = tout.fptr[tid];
+        so_raw[tid] = tout.raw8[tid];
+    }
     // constant chunks of every activation row: [1,1,1,0,...] then zeros
     for (int r = tid; r < G::T; r += kThreads) {
         const float one3[8] = {1.f, 1.f, 1.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -151,36 +153,72 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
 
     // scatter through the `from` map: lane (l%16 = point, l/16 = output
     // group) of wave w holds outputs 4(l/16)..+3 of point w*T/8 + 16n + l%16
-    floatx4 y_prev[G::NB16];
-    int b0_prev = -1;
     const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
-    auto scatter = [&](int bs) {
+    // the output index varies across a wave here: its table entries are
+    // read from an LDS copy
+    auto scatter = [&](int bs, const floatx4 *y) {
         const int q = lane >> 4, pc = lane & 15;
 #pragma unroll
         for (int n = 0; n < G::NB16; ++n) {
             const int b = bs + w * (G::T / 8) + 16 * n + pc;
             const Pt32 pt = locate32(out, b < out.n_points ? b : out.n_points - 1);
-            const bool fast = __all(pt.inside);
+            const uint32_t edge = edge_dims32(out, pt);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int go = 4 * q + r;
                 if (go < pk.f_out && b < out.n_points) {
-                    float v = y_prev[n][r] + pk.bias_out[go];
+                    float v = y[n][r] + pk.bias_out[go];
                     if (orelu)
                         v = fmaxf(v, 0.f);
-                    const FeatureEntry fe = pout.feat[go];
-                    const int32_t idx = fast ? pt.pe + (int32_t)fe.delta : elem32(out, pt, fe);
-                    stg(pout.base[fe.target] + idx, v);
+                    int32_t idx = pt.pe;
+                    if (edge)
+                        idx += edge_fix32(out, pt, so_raw[go], edge);
+                    stg(const_cast<float *>(so_ptr[go]) + idx, v);
                 }
             }
         }
     };
 
+    // ---- gather: (point, chunk) pairs, 8 features per chunk, rounded to
+    //      bf16; features F..F+2 are the constant 1 that carries the
+    //      first-layer bias.  Every pass of a thread has the same point (the
+    //      block size is a multiple of T), so its sweep point is resolved
+    //      once; T is a multiple of 64, so the chunk is wave-uniform and its
+    //      eight feature pointers come from the kernel arguments.  Loads are
+    //      unconditional (table entries past the last feature repeat it;
+    //      unused values are replaced when stored), so all of them are in
+    //      flight before the first use; only the dimensions where the wave
+    //      touches an edge get a boundary fix-up.  The loads of tile t+1 are
+    //      issued before the output layer of tile t and land in registers.
+    constexpr int PASSES = (G::T * 2 * KS1MAX + kThreads - 1) / kThreads;
+    const int gp = tid % G::T;                     // this thread's point in a tile
+    float gv[PASSES][8];
+    bool gvalid = false;
+    auto gather_issue = [&](int tile) {
+        const int b = tile * G::T + gp;
+        gvalid = b < in.n_points;
+        const Pt32 pt = locate32(in, gvalid ? b : in.n_points - 1);
+        const uint32_t edge = edge_dims32(in, pt);
+#pragma unroll
+        for (int it = 0; it < PASSES; ++it) {
+            int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
+            c = c < nchunk_in ? c : nchunk_in - 1;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                int32_t idx = pt.pe;
+                if (edge)
+                    idx += edge_fix32(in, pt, tin.raw8[8 * c + e], edge);
+                gv[it][e] = ldg(tin.fptr[8 * c + e] + idx);
+            }
+        }
+    };
+    if (lb < n_tiles)
+        gather_issue(lb);
+
     for (int tile = lb; tile < n_tiles; tile += nb) {
         const int b0 = tile * G::T;
 
-        // first-layer weight fragments, fetched before the gather so they
-        // arrive while the gather's loads are in flight
+        // first-layer weight fragments
         uint4 a1[KS1MAX][2];
 #pragma unroll
         for (int s = 0; s < KS1MAX; ++s)
@@ -189,49 +227,18 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                 a1[s][j] = s < pk.ks1 ? wload(wr, vlane + j * 1024, (uint32_t)((pk.off_w1 + (int64_t)s * G::NMB * 64) * 16))
                                       : uint4{0u, 0u, 0u, 0u};
 
-        // ---- gather: (point, chunk) pairs, 8 features per chunk, rounded to
-        //      bf16; features F..F+2 are the constant 1 that carries the
-        //      first-layer bias.  Every pass of a thread has the same point
-        //      (the block size is a multiple of T), so its sweep point is
-        //      resolved once; T is a multiple of 64, so the chunk is
-        //      wave-uniform.  Loads are unconditional (feature numbers clamped
-        //      into the plan; unused values replaced afterwards), so all of
-        //      them are in flight before the first use.
-        {
-            constexpr int PASSES = (G::T * 2 * KS1MAX + kThreads - 1) / kThreads;
-            const int p = tid % G::T;
-            const int b = b0 + p;
-            const bool valid = b < in.n_points;
-            const Pt32 pt = locate32(in, valid ? b : in.n_points - 1);
-            const bool fast = __all(pt.inside);          // no boundary resolution anywhere
-            float v[PASSES][8];
+        __syncthreads();                               // the previous tile's output layer is done with Wo
 #pragma unroll
-            for (int it = 0; it < PASSES; ++it) {
-                int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
-                c = c < nchunk_in ? c : nchunk_in - 1;
+        for (int it = 0; it < PASSES; ++it) {
+            const int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
+            float u[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int f = 8 * c + e < F ? 8 * c + e : F - 1;
-                    const FeatureEntry fe = pin.feat[f];
-                    const int32_t idx = fast ? pt.pe + (int32_t)fe.delta : elem32(in, pt, fe);
-                    v[it][e] = ldg(pin.base[fe.target] + idx);
-                }
+            for (int e = 0; e < 8; ++e) {
+                const int f = 8 * c + e;
+                u[e] = f < F ? (gvalid ? gv[it][e] : 0.f) : (f < F + 3 ? 1.f : 0.f);
             }
-            if (b0_prev >= 0)
-                scatter(b0_prev);                        // previous tile's outputs
-            __syncthreads();                             // previous tile's output layer is done with Wo
-#pragma unroll
-            for (int it = 0; it < PASSES; ++it) {
-                const int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
-                float u[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int f = 8 * c + e;
-                    u[e] = f < F ? (valid ? v[it][e] : 0.f) : (f < F + 3 ? 1.f : 0.f);
-                }
-                if (c < nchunk_in)
-                    Xs[p * PX + c] = pack8(u);
-            }
+            if (c < nchunk_in)
+                Xs[gp * PX + c] = pack8(u);
         }
         __syncthreads();
 
@@ -269,18 +276,9 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             const int k = tid + i * kThreads;
             wo_stage[i] = k < KO * 64 ? wload(wr, (uint32_t)(k * 16), (uint32_t)(pk.off_wo * 16)) : uint4{0u, 0u, 0u, 0u};
         }
-        uint4 A[4][2];
-        for (int h = 0; h <= pk.n_hidden; ++h) {
-            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * KT * G::NMB * 64) * 16);
-            auto load_a = [&](uint4 *dst, int s) {
-#pragma unroll
-                for (int j = 0; j < 2; ++j)
-                    dst[j] = wload(wr, vlane + j * 1024, wbase + (uint32_t)s * G::NMB * 1024);
-            };
-            if (h < pk.n_hidden) {
-                load_a(A[0], 0);
-                load_a(A[1], 1);
-            }
+        // epilogue of layer h's accumulators: activation, bf16, into Hs (after
+        // the first layer, also the output-layer fragments into Wo)
+        auto epilogue = [&](int h) {
             __syncthreads();               // every wave is done reading Hs (and Xs)
             if (h == 0) {
 #pragma unroll
@@ -318,8 +316,19 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                         }
             }
             __syncthreads();               // the layer's activations are complete
-            if (h == pk.n_hidden)
-                break;
+        };
+
+        uint4 A[4][2];
+        for (int h = 0; h < pk.n_hidden; ++h) {
+            const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * KT * G::NMB * 64) * 16);
+            auto load_a = [&](uint4 *dst, int s) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    dst[j] = wload(wr, vlane + j * 1024, wbase + (uint32_t)s * G::NMB * 1024);
+            };
+            load_a(A[0], 0);
+            load_a(A[1], 1);
+            epilogue(h);
 
             // K loop, fully unrolled; scheduling barriers pin the pipeline:
             // weight fragments two K-steps ahead (ring of 4), activation
@@ -349,6 +358,11 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
+        // the next tile's gather loads (the last tile re-reads itself, so the
+        // issue is unconditional) land while the last epilogue and the output
+        // layer run
+        gather_issue(tile + nb < n_tiles ? tile + nb : tile);
+        epilogue(pk.n_hidden);
 
         // ---- output layer: 16 x T, K = H on 16x16x32; wave w takes points
         //      [w*T/8, (w+1)*T/8); lane (l%16 = point, l/16 = k group)
@@ -365,22 +379,16 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                     y[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, s == 0 ? floatx4{} : y[n], 0, 0, 0);
                 }
             }
-            // outputs stay in registers; they are scattered after the next
-            // tile's gather loads are issued (or after the loop)
-#pragma unroll
-            for (int n = 0; n < G::NB16; ++n)
-                y_prev[n] = y[n];
-            b0_prev = b0;
+            scatter(b0, y);
         }
         // the next tile's gather stores to Xs after a barrier; Hs is not
         // written again before a barrier
     }
-    if (b0_prev >= 0)
-        scatter(b0_prev);
 }
 
 template <int H, int KS1MAX>
-hipError_t launch_t(const Map32 &in, const Map32 &out, const BF16Packed &pk, hipStream_t stream) {
+hipError_t launch_t(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                    const BF16Packed &pk, hipStream_t stream) {
     using G = Geo<H>;
     const int32_t n_tiles = (in.n_points + G::T - 1) / G::T;
     const size_t xs = (size_t)G::T * (2 * KS1MAX + 1) * 16, wo = (size_t)(H / 32) * 64 * 16;
@@ -390,7 +398,7 @@ hipError_t launch_t(const Map32 &in, const Map32 &out, const BF16Packed &pk, hip
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, stream, in, out, pk, n_tiles);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, stream, in, out, tin, tout, pk, n_tiles);
     return hipGetLastError();
 }
 
@@ -504,13 +512,15 @@ size_t bf16_pack(int n_layers, const int32_t *dims, const float *const *W, const
     return frags.size();
 }
 
-hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const BF16Packed &pk, hipStream_t stream) {
+hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                           const BF16Packed &pk, hipStream_t stream) {
     if (in.n_points == 0)
         return hipSuccess;
     if (pk.hid == 512)
-        return pk.ks1 <= 1 ? launch_t<512, 1>(in, out, pk, stream)
-                           : (pk.ks1 <= 3 ? launch_t<512, 3>(in, out, pk, stream) : launch_t<512, 4>(in, out, pk, stream));
-    return launch_t<256, 1>(in, out, pk, stream);
+        return pk.ks1 <= 1 ? launch_t<512, 1>(in, out, tin, tout, pk, stream)
+                           : (pk.ks1 <= 3 ? launch_t<512, 3>(in, out, tin, tout, pk, stream)
+                                          : launch_t<512, 4>(in, out, tin, tout, pk, stream));
+    return launch_t<256, 1>(in, out, tin, tout, pk, stream);
 }
 
 const char *bf16_variant_name(const BF16Packed &pk) {

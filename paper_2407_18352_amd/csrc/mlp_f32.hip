@@ -83,9 +83,9 @@ __device__ __forceinline__ void load_bias(const float *bias, int g, floatx16 *ac
     }
 }
 
-template <int NMB, int KS1MAX>
-__global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, F32Packed pk,
-                                                      int32_t n_tiles) {
+template <int NMB, int KS1MAX, bool PF>
+__global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout,
+                                                      F32Packed pk, int32_t n_tiles) {
     extern __shared__ float lds[];
     // stage the packed weights once per block
     {
@@ -95,12 +95,6 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, F32Pa
         for (int i = threadIdx.x; i < n4; i += blockDim.x)
             dstl[i] = src[i];
     }
-    __syncthreads();
-
-    __shared__ LdsPlan<64, 64> pin;     // F_in <= 64
-    __shared__ LdsPlan<8, 8> pout;      // F_out <= 8
-    pin.stage(in);
-    pout.stage(out);
     __syncthreads();
 
     const F32Layout lay{NMB, pk.ks1, pk.n_hidden, pk.f_out};
@@ -115,32 +109,53 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, F32Pa
     const int n_waves = nb * waves_per_block;
     const int F = in.n_features;
 
+    // ---- gather: lane (col, g) loads feature 2s+g of its point for K-step
+    //      s.  The two feature pointers of a K-step come from the kernel
+    //      arguments (entries past the last feature repeat it, so the loads
+    //      are unconditional and their count fixed); only the dimensions where
+    //      the wave touches an edge get a boundary fix-up.  The loads of the
+    //      wave's next tile are issued before the current tile's layers run.
+    float xn[KS1MAX];
+    bool nvalid = false;
+    auto gather = [&](int tile) {
+        const int b = tile * 32 + col;
+        nvalid = b < in.n_points;
+        const Pt32 pt = locate32(in, nvalid ? b : in.n_points - 1);
+        const uint32_t edge = edge_dims32(in, pt);
+#pragma unroll
+        for (int s = 0; s < KS1MAX; ++s) {
+            const float *p = g ? tin.fptr[2 * s + 1] : tin.fptr[2 * s];
+            int32_t idx = pt.pe;
+            if (edge)
+                idx += edge_fix32(in, pt, g ? tin.raw8[2 * s + 1] : tin.raw8[2 * s], edge);
+            // (with PF the load count is fixed, so waiting for this tile's
+            // loads never waits for the next tile's)
+            xn[s] = (PF || s < pk.ks1) ? ldg(p + idx) : 0.f;
+            if (s % 8 == 7)
+                __builtin_amdgcn_sched_barrier(0);   // bound the live addresses
+        }
+    };
+    // (without PF -- a wave with a single tile, or the widest variant, which
+    // has no registers for a second set -- each tile is gathered just before
+    // its use)
+    constexpr bool kPrefetch = PF && !(NMB == 4 && KS1MAX == 32);
+    if (kPrefetch && wave_id < n_tiles)
+        gather(wave_id);
+
     for (int tile = wave_id; tile < n_tiles; tile += n_waves) {
         const int b = tile * 32 + col;
-        const bool valid = b < in.n_points;
-
-        // ---- gather: lane (col, g) loads feature 2s+g of point b for K-step s.
-        //      Loads are unconditional (feature numbers clamped into the plan;
-        //      unused values zeroed afterwards) so no branch separates them;
-        //      a wave whose points all read inside the arrays skips boundary
-        //      resolution.
+        if (!kPrefetch)
+            gather(tile);
+        const bool valid = nvalid;
         float x[KS1MAX];
-        {
-            const Pt32 pt = locate32(in, valid ? b : in.n_points - 1);
-            const bool fast = __all(pt.inside);          // no boundary resolution anywhere
 #pragma unroll
-            for (int s = 0; s < KS1MAX; ++s) {
-                const int f = 2 * s + g;
-                const FeatureEntry e = pin.feat[f < F ? f : F - 1];
-                const int32_t idx = fast ? pt.pe + (int32_t)e.delta : elem32(in, pt, e);
-                x[s] = ldg(pin.base[e.target] + idx);
-                if (s % 8 == 7)
-                    __builtin_amdgcn_sched_barrier(0);   // bound the live addresses
-            }
+        for (int s = 0; s < KS1MAX; ++s)
+            x[s] = xn[s];
+        if (kPrefetch)
+            gather(tile + n_waves < n_tiles ? tile + n_waves : tile);
 #pragma unroll
-            for (int s = 0; s < KS1MAX; ++s)
-                x[s] = (valid && 2 * s + g < F) ? x[s] : 0.f;
-        }
+        for (int s = 0; s < KS1MAX; ++s)
+            x[s] = (valid && 2 * s + g < F) ? x[s] : 0.f;
 
         floatx16 acc[NMB];
         // ---- first layer: K = 2 * ks1 (zero-padded features)
@@ -189,6 +204,7 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, F32Pa
 
         // ---- output layer (VALU) + scatter through the `from` map
         const Pt32 po = locate32(out, valid ? b : in.n_points - 1);
+        const uint32_t oedge = edge_dims32(out, po);
         const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
         for (int go = 0; go < pk.f_out; ++go) {
             const float *w = lds + lay.out_w() + (go * 2 + g) * (16 * NMB);
@@ -207,16 +223,15 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, F32Pa
             float y = part + lds[lay.out_b() + go];
             if (orelu)
                 y = fmaxf(y, 0.f);
-            if (g == 0 && valid) {
-                const FeatureEntry e = pout.feat[go];
-                stg(pout.base[e.target] + elem32(out, po, e), y);
-            }
+            if (g == 0 && valid)
+                stg(const_cast<float *>(tout.fptr[go]) + (po.pe + (oedge ? edge_fix32(out, po, tout.raw8[go], oedge) : 0)), y);
         }
     }
 }
 
 template <int NMB, int KS1MAX>
-hipError_t launch_t(const Map32 &in, const Map32 &out, const F32Packed &pk, hipStream_t stream) {
+hipError_t launch_t(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                    const F32Packed &pk, hipStream_t stream) {
     const int32_t n_tiles = (in.n_points + 31) / 32;
     const int threads = NMB == 4 ? 512 : 256;
     const int waves = threads / 64;
@@ -227,11 +242,12 @@ hipError_t launch_t(const Map32 &in, const Map32 &out, const F32Packed &pk, hipS
     const int64_t need = (n_tiles + waves - 1) / waves;
     if (grid > need)
         grid = need;
-    auto kern = mlp_f32_kernel<NMB, KS1MAX>;
+    // prefetch only when waves take more than one tile
+    auto kern = n_tiles > grid * waves ? mlp_f32_kernel<NMB, KS1MAX, true> : mlp_f32_kernel<NMB, KS1MAX, false>;
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, stream, in, out, pk, n_tiles);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, stream, in, out, tin, tout, pk, n_tiles);
     return hipGetLastError();
 }
 
@@ -300,18 +316,23 @@ void f32_pack(int n_layers, const int32_t *dims, const float *const *W, const fl
         img[lay.out_b() + go] = b[n_layers - 1][go];
 }
 
-hipError_t launch_mlp_f32(const Map32 &in, const Map32 &out, const F32Packed &pk, hipStream_t stream) {
+hipError_t launch_mlp_f32(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                          const F32Packed &pk, hipStream_t stream) {
     if (in.n_points == 0)
         return hipSuccess;
     if (pk.hid == 128)
-        return pk.ks1 <= 8 ? launch_t<4, 8>(in, out, pk, stream) : launch_t<4, 32>(in, out, pk, stream);
-    return pk.ks1 <= 8 ? launch_t<2, 8>(in, out, pk, stream) : launch_t<2, 32>(in, out, pk, stream);
+        return pk.ks1 <= 8 ? launch_t<4, 8>(in, out, tin, tout, pk, stream)
+                           : (pk.ks1 <= 20 ? launch_t<4, 20>(in, out, tin, tout, pk, stream)
+                                           : launch_t<4, 32>(in, out, tin, tout, pk, stream));
+    return pk.ks1 <= 8 ? launch_t<2, 8>(in, out, tin, tout, pk, stream)
+                       : (pk.ks1 <= 20 ? launch_t<2, 20>(in, out, tin, tout, pk, stream)
+                                       : launch_t<2, 32>(in, out, tin, tout, pk, stream));
 }
 
 const char *f32_variant_name(const F32Packed &pk) {
     if (pk.hid == 128)
-        return pk.ks1 <= 8 ? "mlp_f32_h128_k16" : "mlp_f32_h128_k64";
-    return pk.ks1 <= 8 ? "mlp_f32_h64_k16" : "mlp_f32_h64_k64";
+        return pk.ks1 <= 8 ? "mlp_f32_h128_k16" : (pk.ks1 <= 20 ? "mlp_f32_h128_k40" : "mlp_f32_h128_k64");
+    return pk.ks1 <= 8 ? "mlp_f32_h64_k16" : (pk.ks1 <= 20 ? "mlp_f32_h64_k40" : "mlp_f32_h64_k64");
 }
 
 }  // namespace hpacml

@@ -171,6 +171,31 @@ def test_infer_fast_paths_are_used():
         assert var.startswith(want), (name, var)
 
 
+@pytest.mark.parametrize("compute, H, F_in, F_out, want", [
+    ("f32", 64, 5, 1, "mlp_f32_h64_k16"), ("f32", 64, 33, 3, "mlp_f32_h64_k40"),
+    ("f32", 64, 57, 8, "mlp_f32_h64_k64"), ("f32", 128, 16, 2, "mlp_f32_h128_k16"),
+    ("f32", 128, 40, 4, "mlp_f32_h128_k40"), ("f32", 128, 64, 1, "mlp_f32_h128_k64"),
+    ("bf16", 256, 13, 16, "mlp_bf16_h256"), ("bf16", 512, 7, 2, "mlp_bf16_h512"),
+    ("bf16", 512, 45, 5, "mlp_bf16_h512"), ("bf16", 512, 61, 9, "mlp_bf16_h512")])
+def test_fast_kernels_input_widths(compute, H, F_in, F_out, want):
+    """Every template variant of the MFMA kernels (input width classes,
+    widths of hidden layers, output counts), pointwise maps with a ragged
+    last tile, against the oracle.  The point counts give every wave (fp32)
+    or block (bf16) more than one tile, so the next tile's gather overlaps
+    the current one's layers."""
+    n = {"f32": 140001, 256: 70001, 512: 40001}[compute if compute == "f32" else H]
+    g = np.random.default_rng(F_in * 1000 + H)
+    spec = wl.pointwise_spec(n)
+    w = wl.Workload("widths", 0, compute, [F_in, H, H, F_out], spec, spec,
+                    [g.uniform(-1, 1, n).astype(np.float32) for _ in range(F_in)],
+                    [wl.sentinel_like((n,)) for _ in range(F_out)])
+    w.model = wl.make_model(F_in + H, w.dims, compute)
+    got, var = run_infer(w)
+    assert var == want, var
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    assert_close(np.stack(got, 1), Y, RTOL[compute], var)
+
+
 def _one_hot_chain(F_in, H, n_hidden, pick, compute):
     """Layer 1 copies input i to hidden unit i; hidden layers copy unit o to
     unit o; the output layer picks input `pick`.  Exact on non-negative inputs."""
