@@ -507,7 +507,7 @@ hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *
             return HPACML_E_ALIAS;
     }
     uint32_t *d = reinterpret_cast<uint32_t *>(dst);
-    return hip_status(m->t32 ? launch_collect32(m->m32, m->tab, d, ld, (hipStream_t)stream)
+    return hip_status(m->t32 ? launch_collect32(m->m32, m->tab, m->plan.pointwise, d, ld, (hipStream_t)stream)
                              : launch_collect(m->dev, d, ld, (hipStream_t)stream));
 }
 

@@ -104,7 +104,9 @@ __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__rest
 // 32-bit form: Map32 view, feature table in the kernel arguments, one tile
 // of 64 * WAVES points per block (no block loops over tiles), and boundary
 // resolution only along the dimensions where the wave touches an edge.
-template <bool DENSE, int WAVES>
+// XCD: order tiles so that each XCD takes a contiguous range (maps with
+// windows share halo lines in that XCD's L2; pointwise maps gain nothing).
+template <bool DENSE, int WAVES, bool XCD>
 __global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTable32 c, uint32_t *__restrict__ dst,
                                                                int64_t ld, uint32_t magic, int32_t n_tiles) {
     extern __shared__ u32x4 tile4[];
@@ -115,7 +117,7 @@ __global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTabl
     // XCD-aware order: the blocks of one XCD (blockIdx % 8) take one
     // contiguous range of tiles, so neighbouring windows share its L2
     const int32_t xq = n_tiles / 8, xr = n_tiles % 8, xx = blockIdx.x % 8;
-    const int32_t tileno = xx * xq + (xx < xr ? xx : xr) + blockIdx.x / 8;
+    const int32_t tileno = XCD ? xx * xq + (xx < xr ? xx : xr) + blockIdx.x / 8 : (int32_t)blockIdx.x;
     const int32_t b0 = tileno * P;
     const int32_t b = b0 + t;
     const Pt32 pt = locate32(m, b < m.n_points ? b : m.n_points - 1);
@@ -163,25 +165,28 @@ __global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTabl
     }
 }
 
-template <bool DENSE, int WAVES>
+template <bool DENSE, int WAVES, bool XCD>
 hipError_t launch_c32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
     constexpr int P = 64 * WAVES;
     const int F = m.n_features;
     const int32_t n_tiles = (int32_t)(((int64_t)m.n_points + P - 1) / P);
     const size_t lds = (size_t)P * F * sizeof(uint32_t);
     const uint32_t magic = (uint32_t)(((1u << 24) + F - 1) / F);
-    hipLaunchKernelGGL((collect32_kernel<DENSE, WAVES>), dim3((unsigned)n_tiles), dim3(P), lds, stream, m, c, dst,
+    hipLaunchKernelGGL((collect32_kernel<DENSE, WAVES, XCD>), dim3((unsigned)n_tiles), dim3(P), lds, stream, m, c, dst,
                        ld, magic, n_tiles);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
+hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, bool pointwise, uint32_t *dst, int64_t ld,
+                            hipStream_t stream) {
     if (m.n_points == 0)
         return hipSuccess;
     const bool dense = ld == m.n_features && ((uintptr_t)dst & 15u) == 0;
-    return dense ? launch_c32<true, 1>(m, c, dst, ld, stream) : launch_c32<false, 1>(m, c, dst, ld, stream);
+    if (pointwise)
+        return dense ? launch_c32<true, 1, false>(m, c, dst, ld, stream) : launch_c32<false, 1, false>(m, c, dst, ld, stream);
+    return dense ? launch_c32<true, 1, true>(m, c, dst, ld, stream) : launch_c32<false, 1, true>(m, c, dst, ld, stream);
 }
 
 hipError_t launch_collect(const DevMap &m, uint32_t *dst, int64_t ld, hipStream_t stream) {

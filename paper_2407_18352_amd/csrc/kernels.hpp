@@ -38,7 +38,8 @@ struct FeatTable32 {
 };
 bool table32_supported(const MapPlan &p, bool map32);
 void table32_make(const MapPlan &p, FeatTable32 *out);
-hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream);
+hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, bool pointwise, uint32_t *dst, int64_t ld,
+                            hipStream_t stream);
 
 // General-shape fused gather -> MLP -> scatter (VALU, any widths).
 hipError_t launch_mlp_generic(const DevMap &in, const DevMap &out, const DevModel &mdl,

@@ -72,22 +72,6 @@ __device__ __forceinline__ uint4 pack8(const float *v) {
     return q;
 }
 
-// ReLU on a packed bf16 pair, with max(x, 0) = 0 for a NaN x as in fp32.
-// As 16-bit integers the values kept are exactly 0x0000..0x7F80 (+0 up to
-// +Inf); every other pattern (negative, -0, NaN of either sign) becomes +0:
-// adding 0x7F sends the positive NaNs past 0x7FFF (negative as int16) and
-// the negative NaNs to 0..0x7E, all of which a signed max with 0x7F then
-// floors.  Rounding and ReLU commute, so this equals rounding max(x, 0).
-typedef short shortx2 __attribute__((ext_vector_type(2)));
-typedef unsigned short ushortx2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t relu2(uint32_t v) {
-    const ushortx2 k = {0x7F, 0x7F};
-    const ushortx2 u = __builtin_bit_cast(ushortx2, v) + k;
-    const shortx2 m = __builtin_elementwise_max(__builtin_bit_cast(shortx2, u), __builtin_bit_cast(shortx2, k));
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(ushortx2, m) - k);
-}
-
-__device__ __forceinline__ uint4 relu8(uint4 q) { return uint4{relu2(q.x), relu2(q.y), relu2(q.z), relu2(q.w)}; }
 
 // feature held at element e of LDS chunk c (C layout of the 32x32 MFMA,
 // two chunks per (m-block, lane half))
@@ -133,11 +117,13 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
     const __amdgpu_buffer_rsrc_t wr = weight_rsrc(pk.frags, pk.frag_bytes);
     const uint32_t vlane = (uint32_t)((m0 * 64 + lane) * 16);
 
-    __shared__ const float *so_ptr[16];             // output table, F_out <= 16
+    __shared__ const float *so_ptr[16];             // output table and biases, F_out <= 16
     __shared__ uint32_t so_raw[16];
+    __shared__ float so_bias[16];
     if (tid < 16) {
         so_ptr[tid] = tout.fptr[tid];
         so_raw[tid] = tout.raw8[tid];
+        so_bias[tid] = pk.bias_out[tid];
     }
     // constant chunks of every activation row: [1,1,1,0,...] then zeros
     for (int r = tid; r < G::T; r += kThreads) {
@@ -154,8 +140,10 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
     // scatter through the `from` map: lane (l%16 = point, l/16 = output
     // group) of wave w holds outputs 4(l/16)..+3 of point w*T/8 + 16n + l%16
     const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
-    // the output index varies across a wave here: its table entries are
-    // read from an LDS copy
+    // the output index varies across a wave here: its table entries and
+    // bias are read from an LDS copy (an indexed kernel argument would be a
+    // vector load, and waiting for it would also wait for the next tile's
+    // gather loads issued before it)
     auto scatter = [&](int bs, const floatx4 *y) {
         const int q = lane >> 4, pc = lane & 15;
 #pragma unroll
@@ -167,7 +155,7 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             for (int r = 0; r < 4; ++r) {
                 const int go = 4 * q + r;
                 if (go < pk.f_out && b < out.n_points) {
-                    float v = y[n][r] + pk.bias_out[go];
+                    float v = y[n][r] + so_bias[go];
                     if (orelu)
                         v = fmaxf(v, 0.f);
                     int32_t idx = pt.pe;
@@ -298,8 +286,8 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                             float v[8];
 #pragma unroll
                             for (int e = 0; e < 8; ++e)
-                                v[e] = acc[j][n][8 * sp + e];
-                            Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = relu8(pack8(v));
+                                v[e] = relu_arith(acc[j][n][8 * sp + e]);
+                            Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = pack8(v);
                         }
             } else {
 #pragma unroll
