@@ -3,7 +3,7 @@
 
 One step = one pass of the whole hot path over the workload: the fused
 gather -> MLP -> scatter (``hpacml_infer``) plus the collect records of the
-region's inputs and outputs (``hpacml_collect`` into a [B x F_in] input
+region's inputs and outputs (``hpacml_collect_pair`` into a [B x F_in] input
 record and a [B x F_out] output record, the two datasets a collected region
 stores).  Inputs are synthetic, seeded and resident in HBM before the timed
 region.  Prints one JSON line.
@@ -123,8 +123,7 @@ def main():
         api.infer(model, mi, mo, stream)
         if ev is not None:
             ev[1].record(stream)
-        api.collect(mi, rec_in, Fi, stream)
-        api.collect(mo_rec, rec_out, Fo, stream)
+        api.collect_pair(mi, rec_in, Fi, mo_rec, rec_out, Fo, stream)
         if ev is not None:
             ev[2].record(stream)
 
@@ -193,7 +192,7 @@ def main():
                              "traffic": collect_traffic["bytes"] if collect_traffic else None,
                              "traffic_source": collect_traffic["source"] if collect_traffic else None,
                              "algorithmic_bytes_per_step": collect_bytes, "ms_per_step": collect_avg,
-                             "kernels": "hpacml_collect of the input map and of the output map"},
+                             "kernels": "hpacml_collect_pair: the input map's and the output map's records"},
         "wall_s_timed": wall,
     }
 

@@ -188,6 +188,19 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in,
  * input/output pairs in one buffer.  Asynchronous on `stream`. */
 hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *stream);
 
+/* Collect mode for a region's two records at once (Sec. IV-B: the mapped
+ * inputs and the outputs are stored as two datasets): the same result as
+ * hpacml_collect(a, dst_a, ld_a) followed by hpacml_collect(b, dst_b, ld_b),
+ * in one launch when both maps allow the library's 32-bit form (else two).
+ * Each argument triple follows hpacml_collect's contract; in addition both
+ * maps are on one device, neither record may overlap a target of either map,
+ * and the two records must be disjoint: byte ranges that do not meet, or one
+ * buffer of equal pitch with disjoint column ranges (dst_b = dst_a + F_a,
+ * ld_a = ld_b >= F_a + F_b) -- anything else is HPACML_E_ALIAS.  Nothing is
+ * enqueued when a check fails.  Asynchronous on `stream`. */
+hpacml_status hpacml_collect_pair(const hpacml_map *a, float *dst_a, int64_t ld_a,
+                                  const hpacml_map *b, float *dst_b, int64_t ld_b, void *stream);
+
 /* Name of the kernel hpacml_infer would launch for these handles (a static
  * string), or NULL when the arguments are invalid. */
 const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in,

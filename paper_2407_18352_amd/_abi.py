@@ -51,6 +51,8 @@ SIGNATURES = {
     "hpacml_model_destroy": (None, [C.c_void_p]),
     "hpacml_infer": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
     "hpacml_collect": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]),
+    "hpacml_collect_pair": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int64,
+                                      C.c_void_p]),
     "hpacml_infer_variant": (C.c_char_p, [C.c_void_p, C.c_void_p, C.c_void_p]),
 }
 

@@ -172,6 +172,18 @@ def collect(m: Map, dst, ld: int, stream=None) -> None:
           "hpacml_collect")
 
 
+def collect_pair(a: Map, dst_a, ld_a: int, b: Map, dst_b, ld_b: int, stream=None) -> None:
+    """``hpacml_collect_pair``: both records of a region in one call (float32
+    device tensors or views)."""
+    import torch
+    for d in (dst_a, dst_b):
+        if d.dtype != torch.float32 or not d.is_cuda:
+            raise TypeError("collect destinations must be float32 device tensors")
+    check(lib().hpacml_collect_pair(a.handle, C.c_void_p(dst_a.data_ptr()), int(ld_a), b.handle,
+                                    C.c_void_p(dst_b.data_ptr()), int(ld_b), _stream(stream)),
+          "hpacml_collect_pair")
+
+
 def variant(model: Model, in_map: Map, out_map: Map) -> str:
     r = lib().hpacml_infer_variant(model.handle, in_map.handle, out_map.handle)
     return r.decode() if r else None

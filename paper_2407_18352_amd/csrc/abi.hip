@@ -234,6 +234,68 @@ void table32_make(const MapPlan &p, FeatTable32 *out) {
 
 }  // namespace hpacml
 
+namespace {
+
+// Bytes a record of n rows x F words with row pitch ld (words) spans.
+int64_t record_bytes(int64_t ld, int32_t F, int64_t n) { return n > 0 ? ((n - 1) * ld + F) * 4 : 0; }
+
+// True when a record may share an element with a target the map reads.
+bool record_overlaps_targets(const hpacml_map *m, const float *dst, int64_t ld, int32_t F, int64_t n) {
+    const char *r0 = (const char *)dst, *r1 = r0 + record_bytes(ld, F, n);
+    for (int t = 0; t < m->plan.n_targets; ++t) {
+        const char *a0 = (const char *)m->plan.base[t];
+        const char *a1 = a0 + 4 * (m->plan.max_elem[t] + 1);
+        if (r0 < a1 && a0 < r1)
+            return true;
+    }
+    return false;
+}
+
+// True when two records may share an element.  Interleaved records of one
+// buffer (same pitch, disjoint column ranges, e.g. inputs in columns 0..8 and
+// the output in column 9) are disjoint.
+bool records_overlap(const float *a, int64_t lda, int32_t Fa, int64_t na, const float *b, int64_t ldb, int32_t Fb,
+                     int64_t nb) {
+    const char *a0 = (const char *)a, *a1 = a0 + record_bytes(lda, Fa, na);
+    const char *b0 = (const char *)b, *b1 = b0 + record_bytes(ldb, Fb, nb);
+    if (a1 <= b0 || b1 <= a0)
+        return false;
+    if (lda != ldb || (b0 - a0) % 4 != 0)
+        return true;
+    const int64_t d = (int64_t)(b0 - a0) / 4;
+    int64_t r = d % lda;
+    if (r < 0)
+        r += lda;
+    return !(Fa <= r && r + Fb <= lda);
+}
+
+// Validation shared by the collect entry points: shape, device, the record
+// inside one device allocation and disjoint from what the map reads.
+hpacml_status check_collect(const hpacml_map *m, float *dst, int64_t ld) {
+    if (!m || !dst)
+        return HPACML_E_INVAL;
+    if (ld < m->plan.n_features)
+        return HPACML_E_SHAPE;
+    if (!same_device(m->device))
+        return HPACML_E_INVAL;
+    if (m->plan.n_points == 0)
+        return HPACML_OK;
+    hipDeviceptr_t abase = nullptr;
+    size_t asize = 0;
+    if (hipMemGetAddressRange(&abase, &asize, (hipDeviceptr_t)dst) != hipSuccess) {
+        (void)hipGetLastError();
+        return HPACML_E_INVAL;
+    }
+    const int64_t need = ((m->plan.n_points - 1) * ld + m->plan.n_features) * 4;
+    if ((const char *)dst + need > (const char *)abase + asize || ((uintptr_t)dst & 3u))
+        return HPACML_E_RANGE;
+    if (record_overlaps_targets(m, dst, ld, m->plan.n_features, m->plan.n_points))
+        return HPACML_E_ALIAS;
+    return HPACML_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int32_t hpacml_abi_version(void) { return HPACML_ABI_VERSION; }
@@ -481,34 +543,46 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
 }
 
 hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *stream) {
-    if (!m || !dst)
-        return HPACML_E_INVAL;
-    if (ld < m->plan.n_features)
-        return HPACML_E_SHAPE;
-    if (!same_device(m->device))
-        return HPACML_E_INVAL;
-    if (m->plan.n_points == 0)
-        return HPACML_OK;
-    // the record must be device memory large enough for every row
-    hipDeviceptr_t abase = nullptr;
-    size_t asize = 0;
-    if (hipMemGetAddressRange(&abase, &asize, (hipDeviceptr_t)dst) != hipSuccess) {
-        (void)hipGetLastError();
-        return HPACML_E_INVAL;
-    }
-    const int64_t need = ((m->plan.n_points - 1) * ld + m->plan.n_features) * 4;
-    if ((const char *)dst + need > (const char *)abase + asize || ((uintptr_t)dst & 3u))
-        return HPACML_E_RANGE;
-    // the record must not overlap what it reads
-    for (int t = 0; t < m->plan.n_targets; ++t) {
-        const char *a0 = (const char *)m->plan.base[t];
-        const char *a1 = a0 + 4 * (m->plan.max_elem[t] + 1);
-        if (!((const char *)dst + need <= a0 || a1 <= (const char *)dst))
-            return HPACML_E_ALIAS;
-    }
+    hpacml_status s = check_collect(m, dst, ld);
+    if (s != HPACML_OK || m->plan.n_points == 0)
+        return s;
     uint32_t *d = reinterpret_cast<uint32_t *>(dst);
-    return hip_status(m->t32 ? launch_collect32(m->m32, m->tab, m->plan.pointwise, d, ld, (hipStream_t)stream)
-                             : launch_collect(m->dev, d, ld, (hipStream_t)stream));
+    if (m->t32) {
+        const CollectJob32 j = collect32_job(m->plan, m->m32, m->tab, d, ld);
+        return hip_status(launch_collect32(&j, 1, (hipStream_t)stream));
+    }
+    return hip_status(launch_collect(m->dev, d, ld, (hipStream_t)stream));
+}
+
+hpacml_status hpacml_collect_pair(const hpacml_map *a, float *dst_a, int64_t ld_a, const hpacml_map *b, float *dst_b,
+                                  int64_t ld_b, void *stream) {
+    hpacml_status s = check_collect(a, dst_a, ld_a);
+    if (s == HPACML_OK)
+        s = check_collect(b, dst_b, ld_b);
+    if (s != HPACML_OK)
+        return s;
+    if (a->device != b->device)
+        return HPACML_E_INVAL;
+    // the one launch reads both maps while it writes both records
+    if (record_overlaps_targets(a, dst_b, ld_b, b->plan.n_features, b->plan.n_points) ||
+        record_overlaps_targets(b, dst_a, ld_a, a->plan.n_features, a->plan.n_points) ||
+        records_overlap(dst_a, ld_a, a->plan.n_features, a->plan.n_points, dst_b, ld_b, b->plan.n_features,
+                        b->plan.n_points))
+        return HPACML_E_ALIAS;
+    uint32_t *da = reinterpret_cast<uint32_t *>(dst_a), *db = reinterpret_cast<uint32_t *>(dst_b);
+    hipStream_t st = (hipStream_t)stream;
+    if (a->t32 && b->t32) {
+        CollectJob32 j[2];
+        int n = 0;
+        if (a->plan.n_points > 0)
+            j[n++] = collect32_job(a->plan, a->m32, a->tab, da, ld_a);
+        if (b->plan.n_points > 0)
+            j[n++] = collect32_job(b->plan, b->m32, b->tab, db, ld_b);
+        return n == 0 ? HPACML_OK : hip_status(launch_collect32(j, n, st));
+    }
+    // maps outside the 32-bit form: two launches, same result
+    s = hpacml_collect(a, dst_a, ld_a, stream);
+    return s == HPACML_OK ? hpacml_collect(b, dst_b, ld_b, stream) : s;
 }
 
 }  // extern "C"

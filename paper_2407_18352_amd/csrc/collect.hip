@@ -102,23 +102,32 @@ __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__rest
 }
 
 // 32-bit form: Map32 view, feature table in the kernel arguments, one tile
-// of 64 * WAVES points per block (no block loops over tiles), and boundary
-// resolution only along the dimensions where the wave touches an edge.
-// XCD: order tiles so that each XCD takes a contiguous range (maps with
-// windows share halo lines in that XCD's L2; pointwise maps gain nothing).
-template <bool DENSE, int WAVES, bool XCD>
-__global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTable32 c, uint32_t *__restrict__ dst,
-                                                               int64_t ld, uint32_t magic, int32_t n_tiles) {
-    extern __shared__ u32x4 tile4[];
+// of 64 points per block (no block loops over tiles), and boundary resolution
+// only along the dimensions where the wave touches an edge.  One launch
+// serves one or two maps (a region's input and output records): the first
+// jobs[0].n_tiles blocks take map 0, the rest map 1.
+//
+// Tile order within a job: blocks of one XCD (blockIdx % 8) take a
+// contiguous range of tiles (windowed maps share halo lines in that XCD's
+// L2; consecutive tiles write consecutive record runs).
+constexpr int kP = 64;   // points per tile (one wave)
+
+// (inlined once per job so that every field is read straight from the
+// kernel arguments: selecting between the two by reference would copy both
+// into private memory)
+__device__ __forceinline__ void collect32_tile(const CollectJob32 &J, int32_t k0, u32x4 *tile4) {
     uint32_t *tile = reinterpret_cast<uint32_t *>(tile4);
-    constexpr int P = 64 * WAVES;
+    const Map32 &m = J.m;
+    const FeatTable32 &c = J.tab;
     const int F = m.n_features;
     const int t = threadIdx.x;
-    // XCD-aware order: the blocks of one XCD (blockIdx % 8) take one
-    // contiguous range of tiles, so neighbouring windows share its L2
-    const int32_t xq = n_tiles / 8, xr = n_tiles % 8, xx = blockIdx.x % 8;
-    const int32_t tileno = XCD ? xx * xq + (xx < xr ? xx : xr) + blockIdx.x / 8 : (int32_t)blockIdx.x;
-    const int32_t b0 = tileno * P;
+    const int32_t n_tiles = J.n_tiles;
+    int32_t tileno = k0;
+    if (J.xcd) {
+        const int32_t xq = n_tiles / 8, xr = n_tiles % 8, xx = k0 % 8;
+        tileno = xx * xq + (xx < xr ? xx : xr) + k0 / 8;
+    }
+    const int32_t b0 = tileno * kP;
     const int32_t b = b0 + t;
     const Pt32 pt = locate32(m, b < m.n_points ? b : m.n_points - 1);
     const uint32_t edge = edge_dims32(m, pt);
@@ -129,17 +138,17 @@ __global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTabl
         uint32_t v[K];
         if (edge == 0) {
 #pragma unroll
-            for (int k = 0; k < K; ++k)
-                v[k] = ldg_bits(c.fptr[fb + k] + pt.pe);
+            for (int e = 0; e < K; ++e)
+                v[e] = ldg_bits(c.fptr[fb + e] + pt.pe);
         } else {
 #pragma unroll
-            for (int k = 0; k < K; ++k)
-                v[k] = ldg_bits(c.fptr[fb + k] + (pt.pe + edge_fix32(m, pt, c.raw8[fb + k], edge)));
+            for (int e = 0; e < K; ++e)
+                v[e] = ldg_bits(c.fptr[fb + e] + (pt.pe + edge_fix32(m, pt, c.raw8[fb + e], edge)));
         }
 #pragma unroll
-        for (int k = 0; k < K; ++k)
-            if (fb + k < F)
-                tile[t * F + fb + k] = v[k];
+        for (int e = 0; e < K; ++e)
+            if (fb + e < F)
+                tile[t * F + fb + e] = v[e];
     };
     int fb = 0;
     for (; fb + 8 <= F; fb += 8)
@@ -148,45 +157,68 @@ __global__ void __launch_bounds__(64 * WAVES) collect32_kernel(Map32 m, FeatTabl
         batch(fb, std::integral_constant<int, 4>{});
     __syncthreads();
 
-    const int rows = (m.n_points - b0) < P ? (m.n_points - b0) : P;
+    const int rows = (m.n_points - b0) < kP ? (m.n_points - b0) : kP;
     const int n = rows * F;                        // words of this tile
-    if (DENSE) {
-        uint32_t *run = dst + (int64_t)b0 * F;     // 16-byte aligned: dst is, P * F is a multiple of 4
-        for (int q = t; q < n / 4; q += P)
+    if (J.dense) {
+        uint32_t *run = J.dst + (int64_t)b0 * F;   // 16-byte aligned: dst is, 64 * F is a multiple of 4
+        for (int q = t; q < n / 4; q += kP)
             stg4(run + 4 * q, tile4[q]);
-        for (int i = (n & ~3) + t; i < n; i += P)
+        for (int i = (n & ~3) + t; i < n; i += kP)
             stg1(run + i, tile[i]);
     } else {
-        for (int i = t; i < n; i += P) {
-            const uint32_t r = div_small((uint32_t)i, magic);
+        for (int i = t; i < n; i += kP) {
+            const uint32_t r = div_small((uint32_t)i, J.magic);
             const uint32_t f = (uint32_t)i - r * (uint32_t)F;
-            stg1(dst + ((int64_t)b0 + r) * ld + f, tile[i]);
+            stg1(J.dst + ((int64_t)b0 + r) * J.ld + f, tile[i]);
         }
     }
 }
 
-template <bool DENSE, int WAVES, bool XCD>
-hipError_t launch_c32(const Map32 &m, const FeatTable32 &c, uint32_t *dst, int64_t ld, hipStream_t stream) {
-    constexpr int P = 64 * WAVES;
-    const int F = m.n_features;
-    const int32_t n_tiles = (int32_t)(((int64_t)m.n_points + P - 1) / P);
-    const size_t lds = (size_t)P * F * sizeof(uint32_t);
-    const uint32_t magic = (uint32_t)(((1u << 24) + F - 1) / F);
-    hipLaunchKernelGGL((collect32_kernel<DENSE, WAVES, XCD>), dim3((unsigned)n_tiles), dim3(P), lds, stream, m, c, dst,
-                       ld, magic, n_tiles);
-    return hipGetLastError();
+__global__ void __launch_bounds__(kP) collect32_kernel(CollectJob32 j0, CollectJob32 j1) {
+    extern __shared__ u32x4 tile4[];
+    if ((int32_t)blockIdx.x < j0.n_tiles)
+        collect32_tile(j0, (int32_t)blockIdx.x, tile4);
+    else
+        collect32_tile(j1, (int32_t)blockIdx.x - j0.n_tiles, tile4);
 }
 
 }  // namespace
 
-hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, bool pointwise, uint32_t *dst, int64_t ld,
-                            hipStream_t stream) {
-    if (m.n_points == 0)
+CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &tab, uint32_t *dst, int64_t ld) {
+    CollectJob32 j{};
+    j.m = m;
+    j.tab = tab;
+    j.dst = dst;
+    j.ld = ld;
+    const int F = p.n_features;
+    j.magic = (uint32_t)(((1u << 24) + F - 1) / F);
+    j.n_tiles = (int32_t)((p.n_points + kP - 1) / kP);
+    j.dense = ld == F && ((uintptr_t)dst & 15u) == 0;
+    j.xcd = !p.pointwise;
+    return j;
+}
+
+hipError_t launch_collect32(const CollectJob32 *jobs, int n_jobs, hipStream_t stream) {
+    // one launch saves a dispatch (several microseconds) where that matters;
+    // large jobs run as separate launches so each gets an LDS tile sized for
+    // its own feature count
+    constexpr int32_t kFuseMaxTiles = 1 << 17;
+    if (n_jobs > 1 && (jobs[0].n_tiles > kFuseMaxTiles || jobs[1].n_tiles > kFuseMaxTiles)) {
+        hipError_t e = launch_collect32(jobs, 1, stream);
+        return e == hipSuccess ? launch_collect32(jobs + 1, 1, stream) : e;
+    }
+    CollectJob32 j0 = jobs[0], j1{};
+    if (n_jobs > 1)
+        j1 = jobs[1];
+    else
+        j1.n_tiles = 0;
+    const int64_t grid = (int64_t)j0.n_tiles + j1.n_tiles;
+    if (grid == 0)
         return hipSuccess;
-    const bool dense = ld == m.n_features && ((uintptr_t)dst & 15u) == 0;
-    if (pointwise)
-        return dense ? launch_c32<true, 1, false>(m, c, dst, ld, stream) : launch_c32<false, 1, false>(m, c, dst, ld, stream);
-    return dense ? launch_c32<true, 1, true>(m, c, dst, ld, stream) : launch_c32<false, 1, true>(m, c, dst, ld, stream);
+    const int fmax = j0.m.n_features > j1.m.n_features ? j0.m.n_features : j1.m.n_features;
+    const size_t lds = (size_t)kP * fmax * sizeof(uint32_t);
+    hipLaunchKernelGGL(collect32_kernel, dim3((unsigned)grid), dim3(kP), lds, stream, j0, j1);
+    return hipGetLastError();
 }
 
 hipError_t launch_collect(const DevMap &m, uint32_t *dst, int64_t ld, hipStream_t stream) {

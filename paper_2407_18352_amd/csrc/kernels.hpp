@@ -38,8 +38,20 @@ struct FeatTable32 {
 };
 bool table32_supported(const MapPlan &p, bool map32);
 void table32_make(const MapPlan &p, FeatTable32 *out);
-hipError_t launch_collect32(const Map32 &m, const FeatTable32 &c, bool pointwise, uint32_t *dst, int64_t ld,
-                            hipStream_t stream);
+// One map's part of a 32-bit collect launch (kernel argument).
+struct CollectJob32 {
+    Map32 m;
+    FeatTable32 tab;
+    uint32_t *dst;
+    int64_t ld;
+    uint32_t magic;      // idx / F by multiply-shift (idx < 2^16)
+    int32_t n_tiles;     // 64-point tiles
+    int32_t dense;       // ld == F and a 16-byte aligned record: one contiguous run per tile
+    int32_t xcd;         // XCD-contiguous tile order (maps with windows)
+};
+CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &tab, uint32_t *dst, int64_t ld);
+// One launch for one or two jobs (n_jobs in {1, 2}).
+hipError_t launch_collect32(const CollectJob32 *jobs, int n_jobs, hipStream_t stream);
 
 // General-shape fused gather -> MLP -> scatter (VALU, any widths).
 hipError_t launch_mlp_generic(const DevMap &in, const DevMap &out, const DevModel &mdl,

@@ -25,7 +25,7 @@ def header_functions():
 
 def test_library_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     L = C.CDLL(_abi.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -190,6 +190,7 @@ def test_model_create_rejects_before_device_work():
     assert st == _abi.E_INVAL and h.value is None
     assert L.hpacml_infer(None, None, None, None) == _abi.E_INVAL
     assert L.hpacml_collect(None, None, 1, None) == _abi.E_INVAL
+    assert L.hpacml_collect_pair(None, None, 1, None, None, 1, None) == _abi.E_INVAL
     assert L.hpacml_infer_variant(None, None, None) is None
     L.hpacml_map_destroy(None)
     L.hpacml_model_destroy(None)

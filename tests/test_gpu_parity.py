@@ -90,6 +90,77 @@ def test_collect_dense_and_offset_records(shape):
     m.close()
 
 
+@pytest.mark.parametrize("name", wl.NAMES)
+def test_collect_pair_matches_two_collects(name):
+    """Both records of a region in one call == the oracle's two records."""
+    import torch
+    w = wl.make(name, "small")
+    outv = [wl.rng(7, 100 + k).uniform(-1, 1, o.shape).astype(np.float32) for k, o in enumerate(w.outputs)]
+    ins, outs = to_dev(w.inputs), to_dev(outv)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.TO)
+    ri = torch.full((mi.n_points, mi.n_features), -1, device="cuda", dtype=torch.int32)
+    ro = torch.full((mo.n_points, mo.n_features), -1, device="cuda", dtype=torch.int32)
+    api.collect_pair(mi, ri.view(torch.float32), mi.n_features, mo, ro.view(torch.float32), mo.n_features)
+    torch.cuda.synchronize()
+    assert np.array_equal(ri.cpu().numpy().view(np.uint32), oracle.collect(w.in_spec, w.inputs))
+    assert np.array_equal(ro.cpu().numpy().view(np.uint32), oracle.collect(w.out_spec, outv))
+
+
+def test_collect_pair_interleaved_record_and_alias():
+    """Inputs in columns 0..8 and the output in column 9 of one [B x 12]
+    record; columns 10, 11 untouched.  Overlapping column ranges are
+    HPACML_E_ALIAS with nothing written."""
+    import torch
+    w = wl.make("bonds", "small")
+    outv = wl.rng(2, 101).uniform(0, 1, w.n_points).astype(np.float32)
+    ins, outs = to_dev(w.inputs), to_dev([outv])
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.TO)
+    rec = torch.full((w.n_points, 12), -1, device="cuda", dtype=torch.int32)
+    rf = rec.view(torch.float32)
+    api.collect_pair(mi, rf, 12, mo, rf[:, 9:], 12)
+    torch.cuda.synchronize()
+    got = rec.cpu().numpy().view(np.uint32)
+    assert np.array_equal(got[:, :9], oracle.collect(w.in_spec, w.inputs))
+    assert np.array_equal(got[:, 9:10], oracle.collect(w.out_spec, [outv]))
+    assert np.all(got[:, 10:] == 0xFFFFFFFF)
+    rec.fill_(-1)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.collect_pair(mi, rf, 12, mo, rf[:, 8:], 12)
+    assert e.value.status == _abi.E_ALIAS
+    torch.cuda.synchronize()
+    assert np.all(rec.cpu().numpy().view(np.uint32) == 0xFFFFFFFF)
+
+
+@pytest.mark.parametrize("shape", [(6, 8, 24), (3, 4, 32), (9, 8, 8)])
+def test_collect_rank3_pair_with_general_map(shape):
+    """Rank-3 windows (one call and the pair call), and a map with an offset
+    beyond a signed byte, which takes the general kernel inside the pair
+    call; all bit-exact."""
+    import torch
+    g = np.random.default_rng(sum(shape))
+    fields = [g.standard_normal(shape).astype(np.float32) for _ in range(2)]
+    spec = wl.sevenpoint3d_spec(*shape)
+    far = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1)), ((0, 0, 130), (1, 1, 1))],
+           "sweep": ((0, 0, 0), shape, (1, 1, 1)), "bnd": [wl.PERIODIC] * 3}
+    dev = to_dev(fields)
+    ma = api.Map(spec, dev, _abi.TO)
+    mb = api.Map(far, dev, _abi.TO)
+    want_a = oracle.collect(spec, fields)
+    want_b = oracle.collect(far, fields)
+    ra = torch.empty((ma.n_points, ma.n_features), device="cuda")
+    rb = torch.empty((mb.n_points, mb.n_features), device="cuda")
+    api.collect(ma, ra, ma.n_features)
+    torch.cuda.synchronize()
+    assert np.array_equal(ra.cpu().numpy().view(np.uint32), want_a)
+    ra.fill_(0)
+    api.collect_pair(ma, ra, ma.n_features, mb, rb, mb.n_features)
+    torch.cuda.synchronize()
+    assert np.array_equal(ra.cpu().numpy().view(np.uint32), want_a)
+    assert np.array_equal(rb.cpu().numpy().view(np.uint32), want_b)
+
+
 @pytest.mark.parametrize("R", [1, 2, 3])
 def test_collect_random_maps_bitexact(R):
     """Random functors, boundary modes, steps, sub-ranges and strided views."""
