@@ -267,6 +267,35 @@ def test_fast_kernels_input_widths(compute, H, F_in, F_out, want):
     assert_close(np.stack(got, 1), Y, RTOL[compute], var)
 
 
+@pytest.mark.parametrize("compute", ["f32", "bf16"])
+def test_limits_max_features_targets_width(compute):
+    """The ABI's maxima in one region: 64 input targets x a 2x2 clamped
+    window = 256 features, a 1024-wide hidden layer, 16 output targets
+    (general kernel); the same map's 256-feature record (64-bit collect)."""
+    import torch
+    g = np.random.default_rng(1024)
+    shape = (23, 31)
+    fields = [g.standard_normal(shape).astype(np.float32) for _ in range(64)]
+    spec = {"rank": 2, "slices": [((0, 0), (2, 2))], "sweep": ((0, 0), shape, (1, 1)),
+            "bnd": [wl.CLAMP, wl.CLAMP]}
+    out_spec = {"rank": 2, "slices": [((0, 0), (1, 1))], "sweep": ((0, 0), shape, (1, 1)),
+                "bnd": [wl.NONE, wl.NONE]}
+    w = wl.Workload("limits", 0, compute, [256, 1024, 16], spec, out_spec, fields,
+                    [wl.sentinel_like(shape) for _ in range(16)])
+    w.model = wl.make_model(5, w.dims, compute)
+    got, var = run_infer(w)
+    assert var.startswith("mlp_generic"), var
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    assert_close(np.stack([a.reshape(-1) for a in got], 1), Y, RTOL[compute], var)
+    m = api.Map(spec, to_dev(fields), _abi.TO)
+    assert m.n_features == 256
+    rec = torch.empty((m.n_points, 256), device="cuda")
+    api.collect(m, rec, 256)
+    torch.cuda.synchronize()
+    assert np.array_equal(rec.cpu().numpy().view(np.uint32), oracle.collect(spec, fields))
+    m.close()
+
+
 def _one_hot_chain(F_in, H, n_hidden, pick, compute):
     """Layer 1 copies input i to hidden unit i; hidden layers copy unit o to
     unit o; the output layer picks input `pick`.  Exact on non-negative inputs."""
