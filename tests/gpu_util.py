@@ -67,6 +67,18 @@ def parity_stats(got, want):
     return float(np.nanmax(ratio)) if ratio.size else 0.0, norm, nan
 
 
+def pure_relative(got, want):
+    """Max |g - o| / |o| over the outputs with |o| >= s (s = the column RMS),
+    where relative error is meaningful."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    s = np.sqrt(np.mean(want * want, axis=0, keepdims=True))
+    mask = np.abs(want) >= s
+    if not mask.any():
+        return 0.0
+    return float(np.max(np.abs(got - want)[mask] / np.abs(want)[mask]))
+
+
 def assert_close(got, want, rtol, what=""):
     worst, norm, nan = parity_stats(got, want)
     assert nan == 0, "%s: %d NaN outputs" % (what, nan)

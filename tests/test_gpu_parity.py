@@ -12,7 +12,7 @@ import pytest
 import oracle
 from paper_2407_18352_amd import _abi, api
 from paper_2407_18352_amd import workloads as wl
-from gpu_util import RTOL, assert_close, require_gpu, run_collect, run_infer, to_dev
+from gpu_util import RTOL, assert_close, parity_stats, pure_relative, require_gpu, run_collect, run_infer, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -208,7 +208,16 @@ def test_infer_small(name):
     gotY = np.stack([a.reshape(-1) for a in got], 1)
     expY = np.stack([a.reshape(-1) for a in exp], 1)
     worst, norm = assert_close(gotY, expY, RTOL[w.compute], "%s via %s" % (name, var))
-    print("%s [%s]: worst %.3e normwise %.3e" % (name, var, worst, norm))
+    line = "%s [%s]: worst scaled %.3e, normwise %.3e, max relative over |o| >= s %.3e" % (
+        name, var, worst, norm, pure_relative(gotY, expY))
+    if w.compute == "bf16":
+        # context, not graded: against the unquantised fp64 model
+        Yf = oracle.infer_rows(w.in_spec, w.inputs, dict(w.model, compute="f32"))
+        expF = [o.copy() for o in w.outputs]
+        oracle.scatter(w.out_spec, expF, Yf)
+        _, normf, _ = parity_stats(gotY, np.stack([a.reshape(-1) for a in expF], 1))
+        line += "; normwise vs the unquantised model %.3e" % normf
+    print(line)
 
 
 @pytest.mark.parametrize("name", wl.NAMES)
