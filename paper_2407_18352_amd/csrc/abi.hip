@@ -168,7 +168,7 @@ DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const 
     return m;
 }
 
-bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev, Map32 *out) {
+bool make_map32(const MapPlan &p, Map32 *out) {
     const int64_t lim = INT32_MAX;
     Map32 m{};
     if (p.n_points >= lim || !p.idx32)
@@ -213,9 +213,6 @@ bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *ba
             if ((uint32_t)(((uint64_t)n * m.magic[d]) >> m.shift[d]) != n / (uint32_t)dv)
                 return false;
     }
-    m.raw8 = p.raw8 ? 1 : 0;
-    m.feat = feat_dev;
-    m.base = base_dev;
     *out = m;
     return true;
 }
@@ -374,7 +371,7 @@ hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir, const hpac
             return s;
         }
         m->dev = make_devmap(m->plan, m->feat_dev, m->base_dev, m->stride_dev);
-        m->fast = make_map32(m->plan, m->feat_dev, m->base_dev, &m->m32);
+        m->fast = make_map32(m->plan, &m->m32);
         m->t32 = table32_supported(m->plan, m->fast);
         if (m->t32)
             table32_make(m->plan, &m->tab);

@@ -151,9 +151,10 @@ __device__ __forceinline__ float round_bf16(float x) {
     return (float)h;
 }
 
-// 32-bit view of a map for the MFMA kernels.  Valid when the point count,
-// every sweep count and every element index fit in int32 and all targets
-// share strides (the common case); maps outside it take the general kernel.
+// 32-bit view of a map for the MFMA and 32-bit collect kernels.  Valid when
+// the point count, every sweep count and every element index fit in int32
+// and all targets share strides (the common case); maps outside it take the
+// general kernels.
 // Division by the sweep counts uses precomputed multipliers: for n < 2^31,
 // n / d == (n * magic) >> shift with shift = 31 + ceil(log2 d) and
 // magic = ceil(2^shift / d).
@@ -164,24 +165,19 @@ struct Map32 {
     int32_t bnd[HPACML_MAX_RANK], omin[HPACML_MAX_RANK], omax[HPACML_MAX_RANK];
     uint32_t magic[HPACML_MAX_RANK];
     int32_t shift[HPACML_MAX_RANK];
-    int32_t raw8;                      // FeatureEntry::raw8 is valid (elem32_edge applies)
-    const FeatureEntry *feat;          // device
-    float *const *base;                // device
 };
 
-// A sweep point resolved for gathering: coordinates, element index in the
-// (shared) strides, and whether every feature's access stays inside.
+// A sweep point resolved for gathering: coordinates and element index in
+// the (shared) strides.
 struct Pt32 {
     int32_t p[HPACML_MAX_RANK];
     int32_t pe;
-    bool inside;
 };
 
 __device__ __forceinline__ Pt32 locate32(const Map32 &m, int32_t b) {
     Pt32 r;
     uint32_t rem = (uint32_t)b;
     r.pe = 0;
-    r.inside = true;
 #pragma unroll
     for (int d = HPACML_MAX_RANK - 1; d >= 0; --d) {
         if (d < m.rank) {
@@ -191,30 +187,11 @@ __device__ __forceinline__ Pt32 locate32(const Map32 &m, int32_t b) {
             const int32_t x = m.start[d] + k * m.step[d];
             r.p[d] = x;
             r.pe += x * m.stride[d];
-            r.inside = r.inside && (x + m.omin[d] >= 0) && (x + m.omax[d] < m.extent[d]);
         } else {
             r.p[d] = 0;
         }
     }
     return r;
-}
-
-// Element index of feature e at point r with boundary resolution, free of
-// divergent branches (both forms computed and selected per lane).
-__device__ __forceinline__ int32_t elem32(const Map32 &m, const Pt32 &r, const FeatureEntry &e) {
-    int32_t res = 0;
-#pragma unroll
-    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
-        if (d < m.rank) {
-            const int32_t n = m.extent[d];
-            const int32_t q = r.p[d] + e.off[d];
-            const int32_t qp = q >= n ? q - n : q;                    // off reduced into [0, n)
-            const int32_t qc = q < 0 ? 0 : (q >= n ? n - 1 : q);
-            const int32_t rr = m.bnd[d] == HPACML_BND_PERIODIC ? qp : (m.bnd[d] == HPACML_BND_CLAMP ? qc : q);
-            res += rr * m.stride[d];
-        }
-    }
-    return r.inside ? r.pe + (int32_t)e.delta : res;
 }
 
 // Dimensions along which some lane of the wave reads outside the arrays:
@@ -271,6 +248,6 @@ struct LdsPlan {
 __host__ DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev,
                             const int64_t *stride_dev);
 // Fills `out` and returns true when the map fits the 32-bit view.
-__host__ bool make_map32(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev, Map32 *out);
+__host__ bool make_map32(const MapPlan &p, Map32 *out);
 
 }  // namespace hpacml
