@@ -98,12 +98,16 @@ template <int H, int KS1MAX>
 __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16Packed pk,
                                                             int32_t n_tiles) {
     using G = Geo<H>;
-    constexpr int PX = 2 * KS1MAX + 1;             // gathered-input row pitch (chunks)
     constexpr int KO = H / 32;                     // output-layer K-steps
     extern __shared__ uint4 smem[];
     uint4 *Hs = smem;                              // [T][PH] activations
-    uint4 *Xs = smem + G::T * G::PH;               // [T][PX] gathered inputs, then
-    uint4 *Wo = Xs;                                //   [KO][64] output-layer fragments
+    // gathered inputs [T][2 KS1MAX] in the first chunks of each activation row:
+    // a row's activations are dead from the previous tile's output layer
+    // until the first layer's epilogue, which comes after the first layer
+    // has read them
+    uint4 *Xs = smem;
+    constexpr int XP = G::PH;                      // Xs row pitch
+    uint4 *Wo = smem + G::T * G::PH;               // [KO][64] output-layer fragments, staged once
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = tid >> 6;
@@ -125,6 +129,9 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
         so_raw[tid] = tout.raw8[tid];
         so_bias[tid] = pk.bias_out[tid];
     }
+    // output-layer fragments, the same for every tile
+    for (int k = tid; k < KO * 64; k += kThreads)
+        Wo[k] = wload(weight_rsrc(pk.frags, pk.frag_bytes), (uint32_t)(k * 16), (uint32_t)(pk.off_wo * 16));
     // constant chunks of every activation row: [1,1,1,0,...] then zeros
     for (int r = tid; r < G::T; r += kThreads) {
         const float one3[8] = {1.f, 1.f, 1.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -200,22 +207,27 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             }
         }
     };
-    if (lb < n_tiles)
-        gather_issue(lb);
-
-    for (int tile = lb; tile < n_tiles; tile += nb) {
-        const int b0 = tile * G::T;
-
-        // first-layer weight fragments
-        uint4 a1[KS1MAX][2];
+    // first-layer weight fragments (the same for every tile), reloaded for
+    // each tile where registers are free: before the last epilogue of the
+    // previous tile, so their latency hides behind it
+    uint4 a1[KS1MAX][2];
+    auto load_a1 = [&]() {
 #pragma unroll
         for (int s = 0; s < KS1MAX; ++s)
 #pragma unroll
             for (int j = 0; j < 2; ++j)
                 a1[s][j] = s < pk.ks1 ? wload(wr, vlane + j * 1024, (uint32_t)((pk.off_w1 + (int64_t)s * G::NMB * 64) * 16))
                                       : uint4{0u, 0u, 0u, 0u};
+    };
+    if (lb < n_tiles) {
+        gather_issue(lb);
+        load_a1();
+    }
 
-        __syncthreads();                               // the previous tile's output layer is done with Wo
+    for (int tile = lb; tile < n_tiles; tile += nb) {
+        const int b0 = tile * G::T;
+
+        __syncthreads();                               // the previous tile's output layer is done with Hs
 #pragma unroll
         for (int it = 0; it < PASSES; ++it) {
             const int c = __builtin_amdgcn_readfirstlane((tid + it * kThreads) / G::T);
@@ -226,7 +238,7 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                 u[e] = f < F ? (gvalid ? gv[it][e] : 0.f) : (f < F + 3 ? 1.f : 0.f);
             }
             if (c < nchunk_in)
-                Xs[gp * PX + c] = pack8(u);
+                Xs[gp * XP + c] = pack8(u);
         }
         __syncthreads();
 
@@ -239,7 +251,7 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             if (s < pk.ks1) {
 #pragma unroll
                 for (int n = 0; n < 4; ++n) {
-                    const bf16x8 bv = as_bf16x8(Xs[(p0 + 32 * n) * PX + 2 * s + g]);
+                    const bf16x8 bv = as_bf16x8(Xs[(p0 + 32 * n) * XP + 2 * s + g]);
 #pragma unroll
                     for (int j = 0; j < 2; ++j)
                         acc[j][n] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -254,28 +266,9 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
         //      output layer) are requested before the epilogue so their L2
         //      latency hides behind it.
         constexpr int KT = G::KS + 1;
-        constexpr int WO_PER_THREAD = (KO * 64 + kThreads - 1) / kThreads;
-        // output-layer fragments for this tile, requested now and stored to
-        // LDS (over the gathered inputs, dead after the first layer) once
-        // every wave is past the first layer
-        uint4 wo_stage[WO_PER_THREAD];
-#pragma unroll
-        for (int i = 0; i < WO_PER_THREAD; ++i) {
-            const int k = tid + i * kThreads;
-            wo_stage[i] = k < KO * 64 ? wload(wr, (uint32_t)(k * 16), (uint32_t)(pk.off_wo * 16)) : uint4{0u, 0u, 0u, 0u};
-        }
-        // epilogue of layer h's accumulators: activation, bf16, into Hs (after
-        // the first layer, also the output-layer fragments into Wo)
+        // epilogue of layer h's accumulators: activation, bf16, into Hs
         auto epilogue = [&](int h) {
             __syncthreads();               // every wave is done reading Hs (and Xs)
-            if (h == 0) {
-#pragma unroll
-                for (int i = 0; i < WO_PER_THREAD; ++i) {
-                    const int k = tid + i * kThreads;
-                    if (k < KO * 64)
-                        Wo[k] = wo_stage[i];
-                }
-            }
             if (pk.act[h] == HPACML_ACT_RELU) {
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
@@ -350,6 +343,7 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
         // issue is unconditional) land while the last epilogue and the output
         // layer run
         gather_issue(tile + nb < n_tiles ? tile + nb : tile);
+        load_a1();
         epilogue(pk.n_hidden);
 
         // ---- output layer: 16 x T, K = H on 16x16x32; wave w takes points
@@ -379,8 +373,8 @@ hipError_t launch_t(const Map32 &in, const Map32 &out, const FeatTable32 &tin, c
                     const BF16Packed &pk, hipStream_t stream) {
     using G = Geo<H>;
     const int32_t n_tiles = (in.n_points + G::T - 1) / G::T;
-    const size_t xs = (size_t)G::T * (2 * KS1MAX + 1) * 16, wo = (size_t)(H / 32) * 64 * 16;
-    const size_t lds = (size_t)G::T * G::PH * 16 + (xs > wo ? xs : wo);
+    static_assert(2 * KS1MAX + 1 <= G::RC, "gathered inputs fit in an activation row");
+    const size_t lds = (size_t)G::T * G::PH * 16 + (size_t)(H / 32) * 64 * 16;
     const int32_t grid = n_tiles < 256 ? n_tiles : 256;
     auto kern = mlp_bf16_kernel<H, KS1MAX>;
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
