@@ -309,10 +309,11 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             };
             load_a(A[0], 0);
             load_a(A[1], 1);
+            load_a(A[2], 2);
             epilogue(h);
 
             // K loop, fully unrolled; scheduling barriers pin the pipeline:
-            // weight fragments two K-steps ahead (ring of 4), activation
+            // weight fragments three K-steps ahead (ring of 4), activation
             // fragments one K-step ahead (ring of 2)
             uint4 Bq[2][4];
             auto load_b = [&](uint4 *dst, int s) {
@@ -323,8 +324,8 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             load_b(Bq[0], 0);
 #pragma unroll
             for (int s = 0; s < KT; ++s) {
-                if (s + 2 < KT)
-                    load_a(A[(s + 2) & 3], s + 2);
+                if (s + 3 < KT)
+                    load_a(A[(s + 3) & 3], s + 3);
                 if (s + 1 < KT)
                     load_b(Bq[(s + 1) & 1], s + 1);
                 __builtin_amdgcn_sched_barrier(0);
