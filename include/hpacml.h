@@ -43,7 +43,7 @@ typedef enum {
     HPACML_E_INVAL = 1,       /* NULL or malformed argument, non-device pointer */
     HPACML_E_SHAPE = 2,       /* feature / point counts do not agree */
     HPACML_E_RANGE = 3,       /* an access leaves an array without a boundary mode */
-    HPACML_E_ALIAS = 4,       /* a `from` target overlaps a `to` target unsafely */
+    HPACML_E_ALIAS = 4,       /* outputs or records that could write one element twice */
     HPACML_E_UNSUPPORTED = 5, /* valid request outside this library's limits */
     HPACML_E_NOMEM = 6,       /* device or host allocation failed */
     HPACML_E_DEVICE = 7       /* HIP runtime error (launch, copy, no device) */
@@ -169,10 +169,19 @@ void hpacml_model_destroy(hpacml_model *m);
 
 /* Inference mode of a region (Sec. III-C `ml(infer)`, Sec. IV-B): for every
  * sweep point, gather through `in` (a TO map), run the model, write the outputs
- * through `out` (a FROM map).  Every point's inputs are read before its
- * outputs are written, and a `from` target may overlap a `to` target only when
- * both maps address exactly the same element per point (same array, zero
- * offsets, same sweep); otherwise HPACML_E_ALIAS.  Requires
+ * through `out` (a FROM map).  The result is that of gathering every point's
+ * inputs before any output is written, also when `from` targets overlap `to`
+ * targets (a region that updates its own fields in place):
+ *   - where both maps address exactly the same element per point (same
+ *     array and strides, zero offsets, same sweep), one fused pass;
+ *   - any other overlap first copies the inputs, as hpacml_collect would,
+ *     into a snapshot record of n_points * features(in) floats that the `in`
+ *     map owns (allocated on first need, freed by hpacml_map_destroy), then
+ *     runs the fused pass on that record.  Inferences that share an `in`
+ *     map share its snapshot: such calls on different streams must not
+ *     overlap in time.
+ * Two `from` targets that can address one element are HPACML_E_ALIAS.
+ * Requires
  * points(in) == points(out), features(in) == dims[0] and
  * features(out) == dims[n_layers] (HPACML_E_SHAPE).  Asynchronous on `stream`;
  * returns HPACML_E_DEVICE only for launch errors.  Zero points: HPACML_OK,
@@ -202,7 +211,8 @@ hpacml_status hpacml_collect_pair(const hpacml_map *a, float *dst_a, int64_t ld_
                                   const hpacml_map *b, float *dst_b, int64_t ld_b, void *stream);
 
 /* Name of the kernel hpacml_infer would launch for these handles (a static
- * string), or NULL when the arguments are invalid. */
+ * string, prefixed "snapshot+" when the inputs are copied first), or NULL
+ * when the arguments are invalid.  Allocates nothing. */
 const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in,
                                  const hpacml_map *out);
 

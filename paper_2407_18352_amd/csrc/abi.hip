@@ -3,6 +3,9 @@
 #include <hip/hip_runtime.h>
 
 #include <cstring>
+#include <mutex>
+#include <set>
+#include <string>
 #include <new>
 #include <vector>
 
@@ -23,6 +26,12 @@ struct hpacml_map_s {
     bool fast = false;   // m32 is valid
     bool t32 = false;    // tab is valid: 32-bit view, raw8, at most 64 features
     FeatTable32 tab{};
+    // snapshot of this (TO) map's inputs for inferences whose outputs may
+    // overwrite them: a [points x features] record and a map over it,
+    // created on first use
+    mutable std::mutex snap_mu;
+    mutable float *snap = nullptr;
+    mutable hpacml_map *snap_map = nullptr;
 };
 
 enum class Variant { Generic, F32, BF16 };
@@ -118,7 +127,8 @@ bool same_device(int dev) {
     return hipGetDevice(&cur) == hipSuccess && cur == dev;
 }
 
-hpacml_status check_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+hpacml_status check_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out,
+                          bool *snapshot = nullptr) {
     if (!model || !in || !out)
         return HPACML_E_INVAL;
     if (in->plan.dir != HPACML_TO || out->plan.dir != HPACML_FROM)
@@ -129,7 +139,12 @@ hpacml_status check_infer(const hpacml_model *model, const hpacml_map *in, const
         return HPACML_E_SHAPE;
     if (in->device != model->device || out->device != model->device || !same_device(model->device))
         return HPACML_E_INVAL;
-    return check_alias(in->plan, out->plan);
+    const Overlap ov = classify_overlap(in->plan, out->plan);
+    if (ov == Overlap::OutputRace)
+        return HPACML_E_ALIAS;
+    if (snapshot)
+        *snapshot = ov == Overlap::Snapshot;
+    return HPACML_OK;
 }
 
 }  // namespace
@@ -337,6 +352,8 @@ void hpacml_map_destroy(hpacml_map *m) {
     (void)hipFree(m->feat_dev);
     (void)hipFree(m->base_dev);
     (void)hipFree(m->stride_dev);
+    hpacml_map_destroy(m->snap_map);
+    (void)hipFree(m->snap);
     delete m;
 }
 
@@ -510,10 +527,79 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
     }
 }
 
-const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
-    if (check_infer(model, in, out) != HPACML_OK)
-        return nullptr;
-    const bool fast = in->t32 && out->t32;
+namespace {
+
+// The snapshot record of a TO map ([points x features], row-major, at `buf`)
+// and the map that reads it back: one rank-2 target [B, F] whose point b
+// reads the row (b, 0..F-1).
+struct SnapshotDesc {
+    hpacml_slice sl{};
+    hpacml_functor fn{};
+    hpacml_array a{};
+    hpacml_sweep sw{};
+    int32_t bnd[HPACML_MAX_RANK] = {HPACML_BND_NONE, HPACML_BND_NONE, HPACML_BND_NONE, HPACML_BND_NONE};
+
+    SnapshotDesc(int64_t B, int32_t F, float *buf) {
+        sl.count[0] = 1;
+        sl.count[1] = F;
+        fn = hpacml_functor{2, 1, &sl, F};
+        a.data = buf;
+        a.dtype = HPACML_F32;
+        a.extent[0] = B;
+        a.extent[1] = F;
+        a.stride[0] = F;
+        a.stride[1] = 1;
+        sw.stop[0] = B;
+        sw.stop[1] = 1;
+        sw.step[0] = sw.step[1] = 1;
+    }
+};
+
+// The snapshot record and its map, allocated on the first inference that
+// needs them (the current device is the map's: check_infer has verified it).
+hpacml_status snapshot_map(const hpacml_map *in, const hpacml_map **out) {
+    std::lock_guard<std::mutex> lock(in->snap_mu);
+    if (!in->snap_map) {
+        const int64_t B = in->plan.n_points;
+        const int32_t F = in->plan.n_features;
+        float *buf = nullptr;
+        hipError_t e = hipMalloc((void **)&buf, (size_t)B * F * sizeof(float));
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            return hip_status(e);
+        }
+        const SnapshotDesc d(B, F, buf);
+        hpacml_map *m = nullptr;
+        hpacml_status s = hpacml_map_create(&d.fn, HPACML_TO, &d.a, 1, &d.sw, d.bnd, &m);
+        if (s != HPACML_OK) {
+            (void)hipFree(buf);
+            return s;
+        }
+        in->snap = buf;
+        in->snap_map = m;
+    }
+    *out = in->snap_map;
+    return HPACML_OK;
+}
+
+// Whether the snapshot map of `in` takes the 32-bit form, without allocating it.
+bool snapshot_t32(const hpacml_map *in) {
+    {
+        std::lock_guard<std::mutex> lock(in->snap_mu);
+        if (in->snap_map)
+            return in->snap_map->t32;
+    }
+    // any non-null address serves the host-side plan
+    const SnapshotDesc d(in->plan.n_points, in->plan.n_features, (float *)in->plan.base[0]);
+    MapPlan p;
+    Map32 m32;
+    if (build_map_plan(&d.fn, HPACML_TO, &d.a, 1, &d.sw, d.bnd, &p) != HPACML_OK)
+        return false;
+    return table32_supported(p, make_map32(p, &m32));
+}
+
+// the kernel the dispatch below picks; `fast` = both maps take the 32-bit form
+const char *kernel_name(const hpacml_model *model, bool fast) {
     switch (fast ? model->variant : Variant::Generic) {
     case Variant::F32: return f32_variant_name(model->f32);
     case Variant::BF16: return bf16_variant_name(model->bf16);
@@ -521,14 +607,46 @@ const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in
     }
 }
 
+// "snapshot+" prefixed names, kept for the life of the process
+const char *snapshot_name(const char *kernel) {
+    static std::mutex mu;
+    static std::set<std::string> names;
+    std::lock_guard<std::mutex> lock(mu);
+    return names.insert(std::string("snapshot+") + kernel).first->c_str();
+}
+
+}  // namespace
+
+const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+    bool snapshot = false;
+    if (check_infer(model, in, out, &snapshot) != HPACML_OK)
+        return nullptr;
+    if (!snapshot)
+        return kernel_name(model, in->t32 && out->t32);
+    return snapshot_name(kernel_name(model, snapshot_t32(in) && out->t32));
+}
+
 hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out,
                            void *stream) {
-    hpacml_status s = check_infer(model, in, out);
+    bool snapshot = false;
+    hpacml_status s = check_infer(model, in, out, &snapshot);
     if (s != HPACML_OK)
         return s;
     if (in->plan.n_points == 0)
         return HPACML_OK;
     hipStream_t st = (hipStream_t)stream;
+    if (snapshot) {
+        // the outputs may overwrite elements that other points still read:
+        // every point's inputs go to the snapshot record first, and the model
+        // then reads them from there (stream order separates the two passes)
+        const hpacml_map *sm = nullptr;
+        s = snapshot_map(in, &sm);
+        if (s == HPACML_OK)
+            s = hpacml_collect(in, in->snap, in->plan.n_features, stream);
+        if (s != HPACML_OK)
+            return s;
+        in = sm;
+    }
     hipError_t e;
     const bool fast = in->t32 && out->t32;
     switch (fast ? model->variant : Variant::Generic) {

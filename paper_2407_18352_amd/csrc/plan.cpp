@@ -275,17 +275,17 @@ bool disjoint_targets(const MapPlan &a, int ta, const MapPlan &b, int tb) {
     return (diff / 4) % smin != 0;
 }
 
-hpacml_status check_alias(const MapPlan &in, const MapPlan &out) {
+Overlap classify_overlap(const MapPlan &in, const MapPlan &out) {
     // two `from` targets that can meet would race
     for (int a = 0; a < out.n_targets; ++a)
         for (int b = a + 1; b < out.n_targets; ++b)
             if (!disjoint_targets(out, a, out, b))
-                return HPACML_E_ALIAS;
+                return Overlap::OutputRace;
     for (int to = 0; to < out.n_targets; ++to)
         for (int ti = 0; ti < in.n_targets; ++ti) {
             if (disjoint_targets(in, ti, out, to))
                 continue;
-            // allowed only as an element-for-element in-place update
+            // safe in one pass only as an element-for-element in-place update
             bool same = in.pointwise && in.base[ti] == out.base[to] && in.rank == out.rank;
             for (int d = 0; same && d < in.rank; ++d) {
                 same = in.stride[(size_t)ti * 4 + d] == out.stride[(size_t)to * 4 + d] &&
@@ -293,9 +293,9 @@ hpacml_status check_alias(const MapPlan &in, const MapPlan &out) {
                        in.count[d] == out.count[d] && out.omin[d] == 0 && out.omax[d] == 0;
             }
             if (!same)
-                return HPACML_E_ALIAS;
+                return Overlap::Snapshot;
         }
-    return HPACML_OK;
+    return Overlap::None;
 }
 
 }  // namespace hpacml

@@ -60,10 +60,14 @@ hpacml_status build_map_plan(const hpacml_functor *f, int32_t dir, const hpacml_
 hpacml_status validate_model(int32_t n_layers, const int32_t *dims, const int32_t *act,
                              int32_t compute);
 
-// Checks that inference with `in` (TO) and `out` (FROM) reads every input
-// before it can be overwritten; HPACML_E_ALIAS when a `from` target may
-// overlap a `to` target other than element-for-element at the same point.
-hpacml_status check_alias(const MapPlan &in, const MapPlan &out);
+// How the targets of an inference's `in` (TO) and `out` (FROM) maps meet.
+enum class Overlap {
+    None,       // disjoint, or a `from` target updates a `to` element-for-element
+    Snapshot,   // a `from` target may overwrite an input another point still
+                // reads: the inputs must be recorded before any output is written
+    OutputRace  // two `from` targets may meet (HPACML_E_ALIAS)
+};
+Overlap classify_overlap(const MapPlan &in, const MapPlan &out);
 
 // True when two targets provably address disjoint elements.
 bool disjoint_targets(const MapPlan &a, int ta, const MapPlan &b, int tb);

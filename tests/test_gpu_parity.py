@@ -422,12 +422,14 @@ def test_errors_are_reported_before_launch():
     with pytest.raises(_abi.HpacmlError) as e:
         api.infer(model, mo, mi)
     assert e.value.status == _abi.E_INVAL
-    # an output overlapping an input other than element-for-element
-    shifted = api.Map(dict(wl.pointwise_spec(999)), [ins[0][1:]], _abi.FROM)
+    # two outputs that can write one element
     mi999 = api.Map(wl.pointwise_spec(999), [x[:999] for x in ins], _abi.TO)
+    two = api.Model(wl.make_model(2, [9, 64, 2], "f32"))
+    racing = api.Map(wl.pointwise_spec(999), [outs[0][:999], outs[0][1:]], _abi.FROM)
     with pytest.raises(_abi.HpacmlError) as e:
-        api.infer(model, mi999, shifted)
+        api.infer(two, mi999, racing)
     assert e.value.status == _abi.E_ALIAS
+    assert api.variant(two, mi999, racing) is None
     # element-for-element in place is allowed
     inplace = api.Map(w.out_spec, [ins[3]], _abi.FROM)
     api.infer(model, mi, inplace)
@@ -463,7 +465,8 @@ def test_errors_are_reported_before_launch():
 
 
 def test_inplace_pointwise_matches_oracle():
-    """Element-for-element in-place update: the output overwrites input 0."""
+    """Element-for-element in-place update: the output overwrites input 0 in
+    one pass (each point reads its own element before writing it)."""
     import torch
     w = wl.make("options", 5000)
     Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
@@ -471,6 +474,78 @@ def test_inplace_pointwise_matches_oracle():
     mi = api.Map(w.in_spec, ins, _abi.TO)
     mo = api.Map(w.out_spec, [ins[0]], _abi.FROM)
     m = api.Model(w.model)
+    assert not api.variant(m, mi, mo).startswith("snapshot+")
     api.infer(m, mi, mo)
     torch.cuda.synchronize()
     assert_close(ins[0].cpu().numpy()[:, None], Y, RTOL["f32"], "in place")
+
+
+def test_inplace_shifted_output_reads_snapshot():
+    """Outputs written one element past the inputs they overwrite: point b's
+    output lands on point b+1's input, which must still be read as it was."""
+    import torch
+    w = wl.make("bonds", 999)
+    big = [np.concatenate([a, np.float32([0.5])]) for a in w.inputs]
+    ins = to_dev(big)
+    mi = api.Map(wl.pointwise_spec(999), [x[:999] for x in ins], _abi.TO)
+    mo = api.Map(wl.pointwise_spec(999), [ins[0][1:]], _abi.FROM)
+    m = api.Model(w.model)
+    var = api.variant(m, mi, mo)
+    assert var.startswith("snapshot+mlp_f32"), var
+    exp = [a.copy() for a in big]
+    Y = oracle.infer_rows(wl.pointwise_spec(999), [a[:999] for a in exp], w.model)
+    exp[0][1:] = Y[:, 0]
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    got = ins[0].cpu().numpy()
+    assert got[0] == big[0][0]
+    assert_close(got[1:, None], exp[0][1:, None], RTOL["f32"], "shifted in place via " + var)
+
+
+@pytest.mark.parametrize("name, size, steps", [("stencil2d", (20, 40), 2), ("stencil2d", (3, 130), 1),
+                                               ("stencil3d", (6, 7, 9), 1)])
+def test_inplace_window_update_reads_snapshot(name, size, steps):
+    """A stencil region that writes its results back into the fields its
+    windows read (a time step advanced in place).  Every point's window is
+    read before any output is written, so each step equals the oracle's
+    region (all gathers, then the model, then all scatters) on the same
+    arrays; later steps reuse the map's snapshot record."""
+    import torch
+    w = wl.make(name, size)
+    fields = to_dev(w.inputs)
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.Model(w.model)
+    var = api.variant(m, mi, mo)
+    assert var.startswith("snapshot+mlp_" + w.compute), var
+    exp = [a.copy() for a in w.inputs]
+    for _ in range(steps):
+        api.infer(m, mi, mo)
+        oracle.infer(w.in_spec, exp, w.out_spec, exp, w.model)
+    torch.cuda.synchronize()
+    got = np.stack([f.cpu().numpy().reshape(-1) for f in fields], 1)
+    want = np.stack([a.reshape(-1) for a in exp], 1)
+    worst, norm = assert_close(got, want, RTOL[w.compute], "%s in place via %s" % (name, var))
+    print("%s %s in place, %d steps [%s]: worst scaled %.3e, normwise %.3e" % (name, size, steps, var, worst,
+                                                                                norm))
+
+
+def test_inplace_window_update_general_maps():
+    """The same in-place stencil step with one field stored transposed: the
+    targets' strides differ, so both maps take the general (64-bit) form."""
+    import torch
+    w = wl.make("stencil2d", (12, 20))
+    fields = to_dev(w.inputs)
+    fields[1] = torch.from_numpy(np.ascontiguousarray(w.inputs[1].T)).cuda().t()
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.Model(w.model)
+    var = api.variant(m, mi, mo)
+    assert var == "snapshot+mlp_generic_f32", var
+    exp = [a.copy() for a in w.inputs]
+    api.infer(m, mi, mo)
+    oracle.infer(w.in_spec, exp, w.out_spec, exp, w.model)
+    torch.cuda.synchronize()
+    got = np.stack([f.cpu().numpy().reshape(-1) for f in fields], 1)
+    want = np.stack([a.reshape(-1) for a in exp], 1)
+    assert_close(got, want, RTOL["f32"], "general in place via " + var)
