@@ -18,6 +18,12 @@ plain data:
   strides are taken from the arrays.
 * model spec: ``{"dims": [...], "W": [...], "b": [...], "act": [...],
   "compute": "f32" | "bf16"}`` with ``W[l]`` of shape ``[dims[l+1], dims[l]]``.
+* convolutional model spec: ``{"kind": "cnn", "in_channels": C, "image": (H, W),
+  "layers": [...]}``, each layer ``{"kind": "conv" | "pool" | "linear", "out",
+  "kernel", "stride", "padding": "same" | "valid", "mode": "zeros" | "circular"
+  | "replicate", "act", "W", "b"}`` (conv ``W`` is ``[out, in, kh, kw]``,
+  linear ``W`` is ``[out, in]`` over the flattened [row][column][channel]
+  input).
 """
 from __future__ import annotations
 
@@ -59,6 +65,18 @@ class _Map(C.Structure):
                 ("data", C.POINTER(C.c_void_p)), ("stride", C.POINTER(C.c_int64))]
 
 
+class _Layer(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("out_channels", C.c_int32), ("kh", C.c_int32), ("kw", C.c_int32),
+                ("sh", C.c_int32), ("sw", C.c_int32), ("padding", C.c_int32), ("pad_mode", C.c_int32),
+                ("act", C.c_int32), ("pad_", C.c_int32),
+                ("W", C.POINTER(C.c_float)), ("b", C.POINTER(C.c_float))]
+
+
+LAYER_KIND = {"conv": 0, "pool": 1, "linear": 2}
+PADDING = {"valid": 0, "same": 1}
+PAD_MODE = {"zeros": 0, "circular": 1, "replicate": 2}
+
+
 class _Model(C.Structure):
     _fields_ = [("n_layers", C.c_int32), ("bf16", C.c_int32),
                 ("dims", C.POINTER(C.c_int32)), ("W", C.POINTER(C.POINTER(C.c_float))),
@@ -84,7 +102,11 @@ def lib():
             L.or_mlp.argtypes = [P(_Model), P(C.c_double), C.c_int64, P(C.c_float)]
             L.or_infer_rows.argtypes = [P(_Map), P(_Model), P(C.c_int64), C.c_int64, P(C.c_float)]
             L.or_scatter.argtypes = [P(_Map), P(C.c_int64), C.c_int64, P(C.c_float)]
-            for fn in (L.or_gather, L.or_collect, L.or_mlp, L.or_infer_rows, L.or_scatter):
+            L.or_cnn_shapes.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, P(_Layer), P(C.c_int32)]
+            L.or_cnn.argtypes = [C.c_int32, C.c_int32, C.c_int32, C.c_int32, P(_Layer), P(C.c_double),
+                                 C.c_int64, P(C.c_float)]
+            for fn in (L.or_gather, L.or_collect, L.or_mlp, L.or_infer_rows, L.or_scatter, L.or_cnn_shapes,
+                       L.or_cnn):
                 fn.restype = C.c_int
             _lib = L
     return _lib
@@ -158,6 +180,54 @@ def _model(spec) -> _Keep:
     m.W = C.cast(Wp, C.POINTER(C.POINTER(C.c_float)))
     m.b = C.cast(bp, C.POINTER(C.POINTER(C.c_float)))
     return _Keep(m, dims, Ws, bs, act, Wp, bp)
+
+
+def _layers(model) -> _Keep:
+    Ls = model["layers"]
+    arr = (_Layer * len(Ls))()
+    keep = []
+    for i, ly in enumerate(Ls):
+        a = arr[i]
+        a.kind = LAYER_KIND[ly["kind"]]
+        a.out_channels = int(ly.get("out", 0))
+        a.kh, a.kw = (int(v) for v in ly.get("kernel", (1, 1)))
+        # default steps: 1 for a convolution, the window for a pool (PyTorch's defaults)
+        a.sh, a.sw = (int(v) for v in ly.get("stride", ly.get("kernel") if ly["kind"] == "pool" else (1, 1)))
+        a.padding = PADDING[ly.get("padding", "valid")]
+        a.pad_mode = PAD_MODE[ly.get("mode", "zeros")]
+        a.act = int(ly.get("act", 0))
+        if ly["kind"] != "pool":
+            W = np.ascontiguousarray(ly["W"], np.float32)
+            b = np.ascontiguousarray(ly["b"], np.float32)
+            keep += [W, b]
+            a.W, a.b = _ptr(W, C.c_float), _ptr(b, C.c_float)
+    return _Keep(arr, keep)
+
+
+def cnn_shapes(model) -> list:
+    """(rows, columns, channels) of every layer's input and of the output."""
+    k = _layers(model)
+    L = len(model["layers"])
+    sh = np.zeros(3 * (L + 1), np.int32)
+    H, W = model["image"]
+    _check(lib().or_cnn_shapes(model["in_channels"], H, W, L, k.s, _ptr(sh, C.c_int32)), "cnn shapes")
+    return [tuple(int(v) for v in sh[3 * l: 3 * l + 3]) for l in range(L + 1)]
+
+
+def cnn(model, X) -> np.ndarray:
+    """Convolutional model on composed tensors X[S*H*W, C] (S images in sweep
+    order) -> float32 Y[S*H'*W', C']."""
+    k = _layers(model)
+    L = len(model["layers"])
+    H, W = model["image"]
+    C0 = model["in_channels"]
+    X = np.ascontiguousarray(X, np.float64)
+    assert X.ndim == 2 and X.shape[1] == C0 and X.shape[0] % (H * W) == 0
+    S = X.shape[0] // (H * W)
+    h2, w2, c2 = cnn_shapes(model)[-1]
+    Y = np.zeros((S * h2 * w2, c2), np.float32)
+    _check(lib().or_cnn(C0, H, W, L, k.s, _ptr(X, C.c_double), S, _ptr(Y, C.c_float)), "cnn")
+    return Y
 
 
 def _rows(rows):
@@ -249,7 +319,10 @@ def scatter(spec, targets, Y, rows=None) -> None:
 def infer(in_spec, in_targets, out_spec, out_targets, model) -> np.ndarray:
     """The whole region: every gather, then the model, then every scatter.
     Returns Y and writes the `from` targets in place."""
-    Y = infer_rows(in_spec, in_targets, model)
+    if model.get("kind") == "cnn":
+        Y = cnn(model, gather(in_spec, in_targets))
+    else:
+        Y = infer_rows(in_spec, in_targets, model)
     scatter(out_spec, out_targets, Y)
     return Y
 

@@ -19,7 +19,11 @@
  *   4. the output tensor is written back through a `from` map, which performs
  *      extraction, resolution and wrapping but no composition (Sec. IV-A, last
  *      paragraph);
- *   5. collect mode records the mapped values instead (Sec. III-A-2, IV-B).
+ *   5. collect mode records the mapped values instead (Sec. III-A-2, IV-B);
+ *   6. convolutional surrogates (the MiniWeather and ParticleFilter model
+ *      spaces of Table VI: convolution, max-pool and fully connected layers)
+ *      run on the composed tensor seen as images: the last two sweep
+ *      dimensions are the image rows and columns, the features its channels.
  *
  * Arithmetic is fp64 with sequential summation.  Where the paper is silent the
  * readings are (each is listed in the design notes):
@@ -32,7 +36,13 @@
  *     identity or ReLU (hidden layers ReLU, output linear);
  *   - bf16 models: weights, gathered inputs and hidden activations rounded to
  *     bf16 (round to nearest even) after an fp32 rounding; biases and outputs
- *     stay fp32.
+ *     stay fp32;
+ *   - convolution: PyTorch's Conv2d definition (weights [out][in][kh][kw],
+ *     cross-correlation), "same" padding split as floor((k-1)/2) before and
+ *     the rest after, padding modes zeros / circular / replicate; max-pool
+ *     without padding, NaN if any window value is NaN; a fully connected
+ *     layer flattens its input image in [row][column][channel] order (the
+ *     composed tensor's own order).
  *
  * Every function here is pinned by tests that do not re-type its formula:
  * brute-force numpy enumeration with np.pad wrap/edge, the paper's 5-point
@@ -446,4 +456,169 @@ int or_scatter(const or_map *m, const int64_t *rows, int64_t n, const float *Y)
     free(tgt);
     free(elem);
     return err;
+}
+
+/* ---- convolutional surrogates ---------------------------------------------
+ * The composed tensor X[S][H][W][C0] (sweep order: leading sweep dimensions
+ * number the S images, the last two are the rows and columns, the features
+ * are the channels) passes through the layers in order. */
+enum { OR_CONV2D = 0, OR_MAXPOOL2D = 1, OR_LINEAR = 2 };
+enum { OR_PAD_VALID = 0, OR_PAD_SAME = 1 };
+enum { OR_PM_ZEROS = 0, OR_PM_CIRCULAR = 1, OR_PM_REPLICATE = 2 };
+
+typedef struct {
+    int32_t kind;
+    int32_t out_channels;  /* conv: output channels; linear: outputs */
+    int32_t kh, kw;        /* window */
+    int32_t sh, sw;        /* steps */
+    int32_t padding;       /* conv: valid / same */
+    int32_t pad_mode;      /* conv with same padding */
+    int32_t act;           /* 0 identity, 1 ReLU */
+    int32_t pad_;
+    const float *W;        /* conv [out][in][kh][kw]; linear [out][in]; pool NULL */
+    const float *b;        /* [out]; pool NULL */
+} or_layer;
+
+/* Image shape after every layer: shape[3l..3l+2] = (rows, columns, channels)
+ * of layer l's input, l = 0..L (entry L is the output). */
+int or_cnn_shapes(int32_t C0, int32_t H, int32_t W, int32_t L, const or_layer *ly, int32_t *shape)
+{
+    if (C0 < 1 || H < 1 || W < 1 || L < 1)
+        return OR_ERR_ARG;
+    int32_t h = H, w = W, c = C0;
+    int flat = 0;
+    shape[0] = h, shape[1] = w, shape[2] = c;
+    for (int l = 0; l < L; ++l) {
+        const or_layer *y = &ly[l];
+        if (y->kind == OR_LINEAR) {
+            c = y->out_channels;
+            h = w = 1;
+            flat = 1;
+        } else {
+            if (flat || y->kh < 1 || y->kw < 1 || y->sh < 1 || y->sw < 1)
+                return OR_ERR_ARG;
+            if (y->kind == OR_CONV2D && y->padding == OR_PAD_SAME) {
+                if (y->sh != 1 || y->sw != 1)
+                    return OR_ERR_ARG;
+            } else {
+                if (y->kh > h || y->kw > w)
+                    return OR_ERR_ARG;
+                h = (h - y->kh) / y->sh + 1;
+                w = (w - y->kw) / y->sw + 1;
+            }
+            if (y->kind == OR_CONV2D)
+                c = y->out_channels;
+        }
+        if (c < 1)
+            return OR_ERR_ARG;
+        shape[3 * (l + 1)] = h, shape[3 * (l + 1) + 1] = w, shape[3 * (l + 1) + 2] = c;
+    }
+    return OR_OK;
+}
+
+/* Input row or column q of a same-padded convolution, q possibly outside
+ * [0, n): its index inside, or -1 for a zero (zeros mode). */
+static int64_t pad_index(int64_t q, int64_t n, int mode)
+{
+    if (q >= 0 && q < n)
+        return q;
+    if (mode == OR_PM_CIRCULAR)
+        return ((q % n) + n) % n;
+    if (mode == OR_PM_REPLICATE)
+        return q < 0 ? 0 : n - 1;
+    return -1;
+}
+
+/* One layer on S images in[S][h][w][c] -> out[S][h2][w2][c2]. */
+static void cnn_layer(const or_layer *y, const double *in, int64_t S, int h, int w, int c, double *out,
+                      int h2, int w2, int c2)
+{
+    int64_t n_out = S * h2 * w2;
+    int64_t i;
+#pragma omp parallel for schedule(static)
+    for (i = 0; i < n_out; ++i) {
+        int64_t s = i / ((int64_t)h2 * w2);
+        int oy = (int)(i / w2 % h2), ox = (int)(i % w2);
+        const double *img = in + s * h * w * c;
+        double *o = out + i * c2;
+        if (y->kind == OR_CONV2D) {
+            /* out[co] = b[co] + sum over ci, ky, kx of W[co][ci][ky][kx] * in[y0 + ky][x0 + kx][ci] */
+            int same = y->padding == OR_PAD_SAME;
+            int64_t y0 = (int64_t)oy * y->sh - (same ? (y->kh - 1) / 2 : 0);
+            int64_t x0 = (int64_t)ox * y->sw - (same ? (y->kw - 1) / 2 : 0);
+            for (int co = 0; co < c2; ++co) {
+                double acc = (double)y->b[co];
+                for (int ci = 0; ci < c; ++ci)
+                    for (int ky = 0; ky < y->kh; ++ky) {
+                        int64_t r = same ? pad_index(y0 + ky, h, y->pad_mode) : y0 + ky;
+                        for (int kx = 0; kx < y->kw; ++kx) {
+                            int64_t q = same ? pad_index(x0 + kx, w, y->pad_mode) : x0 + kx;
+                            double v = (r < 0 || q < 0) ? 0.0 : img[(r * w + q) * c + ci];
+                            acc += (double)y->W[(((int64_t)co * c + ci) * y->kh + ky) * y->kw + kx] * v;
+                        }
+                    }
+                o[co] = y->act == 1 ? (acc > 0.0 ? acc : 0.0) : acc;
+            }
+        } else if (y->kind == OR_MAXPOOL2D) {
+            /* the largest window value; a NaN anywhere in the window wins */
+            const double *win = img + ((int64_t)oy * y->sh * w + (int64_t)ox * y->sw) * c;
+            for (int ch = 0; ch < c2; ++ch) {
+                double m = win[ch];
+                for (int ky = 0; ky < y->kh; ++ky)
+                    for (int kx = 0; kx < y->kw; ++kx) {
+                        double v = win[((int64_t)ky * w + kx) * c + ch];
+                        if (!isnan(m) && (isnan(v) || v > m))
+                            m = v;
+                    }
+                o[ch] = y->act == 1 ? (m > 0.0 ? m : 0.0) : m;
+            }
+        } else {
+            /* the image flattened in [row][column][channel] order */
+            int64_t n_in = (int64_t)h * w * c;
+            for (int oo = 0; oo < c2; ++oo) {
+                double acc = (double)y->b[oo];
+                for (int64_t k = 0; k < n_in; ++k)
+                    acc += (double)y->W[(int64_t)oo * n_in + k] * img[k];
+                o[oo] = y->act == 1 ? (acc > 0.0 ? acc : 0.0) : acc;
+            }
+        }
+    }
+}
+
+/* The whole stack on X[S][H][W][C0] (fp64) -> Y[S][H'][W'][C'] rounded to fp32. */
+int or_cnn(int32_t C0, int32_t H, int32_t W, int32_t L, const or_layer *ly, const double *X, int64_t S,
+           float *Y)
+{
+    int32_t shape[3 * 65];
+    if (L > 64)
+        return OR_ERR_ARG;
+    int rc = or_cnn_shapes(C0, H, W, L, ly, shape);
+    if (rc != OR_OK)
+        return rc;
+    int64_t big = 0;
+    for (int l = 0; l <= L; ++l) {
+        int64_t n = (int64_t)shape[3 * l] * shape[3 * l + 1] * shape[3 * l + 2];
+        big = n > big ? n : big;
+    }
+    double *a = malloc(sizeof(double) * (size_t)(S * big + 1));
+    double *bb = malloc(sizeof(double) * (size_t)(S * big + 1));
+    if (!a || !bb) {
+        free(a);
+        free(bb);
+        return OR_ERR_NOMEM;
+    }
+    memcpy(a, X, sizeof(double) * (size_t)(S * H * W * C0));
+    for (int l = 0; l < L; ++l) {
+        const int32_t *si = shape + 3 * l, *so = shape + 3 * (l + 1);
+        cnn_layer(&ly[l], a, S, si[0], si[1], si[2], bb, so[0], so[1], so[2]);
+        double *t = a;
+        a = bb;
+        bb = t;
+    }
+    int64_t n = S * (int64_t)shape[3 * L] * shape[3 * L + 1] * shape[3 * L + 2];
+    for (int64_t i = 0; i < n; ++i)
+        Y[i] = (float)a[i];
+    free(a);
+    free(bb);
+    return OR_OK;
 }
