@@ -30,13 +30,14 @@
 extern "C" {
 #endif
 
-#define HPACML_ABI_VERSION 1
+#define HPACML_ABI_VERSION 2
 #define HPACML_MAX_RANK 4         /* spatial dimensions of a functor / sweep */
 #define HPACML_MAX_SLICES 64      /* right-hand-side slices per functor */
 #define HPACML_MAX_TARGETS 64     /* arrays per map */
 #define HPACML_MAX_FEATURES 256   /* features per point of one map */
 #define HPACML_MAX_LAYERS 8       /* layers per model */
 #define HPACML_MAX_WIDTH 1024     /* width of any layer */
+#define HPACML_MAX_CNN_WIDTH 65536 /* channels of a convolutional layer, inputs of a LINEAR layer */
 
 typedef enum {
     HPACML_OK = 0,
@@ -166,6 +167,74 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims,
 
 /* Frees a model.  NULL-safe.  Synchronise streams that use it first. */
 void hpacml_model_destroy(hpacml_model *m);
+
+/* ---- convolutional surrogates --------------------------------------------
+ * The models the paper searches for image-shaped regions (Table VI:
+ * MiniWeather's one or two convolution layers of 4-8 channels, ParticleFilter's
+ * convolution, max-pool and fully connected layers) run on the composed input
+ * tensor seen as S images: the last two sweep dimensions of the `to` map are
+ * the image rows and columns (the counts must equal `height`, `width`), any
+ * leading sweep dimensions number the images, and the map's features are the
+ * channels.  The result, [S][rows'][columns'][channels'] in that order, is
+ * written through the `from` map, whose points must number S * rows' *
+ * columns' and whose features must equal channels'. */
+enum { HPACML_LAYER_CONV2D = 0, HPACML_LAYER_MAXPOOL2D = 1, HPACML_LAYER_LINEAR = 2 };
+/* convolution padding: VALID (none: the output shrinks by window - 1) or SAME
+ * (the output keeps the input's size; floor((k-1)/2) rows/columns of padding
+ * before, the rest after; stride must be 1) */
+enum { HPACML_PAD_VALID = 0, HPACML_PAD_SAME = 1 };
+/* what SAME padding reads outside the image: zeros, the opposite edge
+ * (wrapping as often as needed), or the nearest edge element */
+enum { HPACML_PADMODE_ZEROS = 0, HPACML_PADMODE_CIRCULAR = 1, HPACML_PADMODE_REPLICATE = 2 };
+
+/* One layer of a convolutional model.
+ *   CONV2D:    out[y][x][co] = b[co] + sum over ci, ky, kx of
+ *              W[co][ci][ky][kx] * in[y*stride[0] + ky - pad_top][x*stride[1] + kx - pad_left][ci]
+ *              (PyTorch Conv2d weights, cross-correlation); out_channels >= 1.
+ *   MAXPOOL2D: out[y][x][c] = max over the kernel window at (y*stride[0], x*stride[1]),
+ *              no padding, NaN when any window value is NaN; out_channels unused.
+ *   LINEAR:    the image flattened in [row][column][channel] order, then
+ *              out[o] = b[o] + sum_i W[o][i] in[i]; the result is a 1 x 1 image
+ *              of out_channels channels.  Only LINEAR layers may follow a LINEAR.
+ * `act` (HPACML_ACT_*) applies to every layer's output.  kernel and stride
+ * entries are >= 1; VALID windows must fit the layer's input. */
+typedef struct {
+    int32_t kind;            /* HPACML_LAYER_* */
+    int32_t out_channels;    /* CONV2D: output channels; LINEAR: outputs */
+    int32_t kernel[2];       /* CONV2D / MAXPOOL2D window: rows, columns */
+    int32_t stride[2];       /* CONV2D / MAXPOOL2D step: rows, columns */
+    int32_t padding;         /* CONV2D: HPACML_PAD_* */
+    int32_t pad_mode;        /* CONV2D with SAME: HPACML_PADMODE_* */
+    int32_t act;             /* HPACML_ACT_* */
+} hpacml_layer;
+
+/* Checks a convolutional model description without touching any device.
+ * in_channels: 1..HPACML_MAX_FEATURES; height, width >= 1; n_layers
+ * 1..HPACML_MAX_LAYERS; every layer's channels (and a LINEAR layer's inputs)
+ * <= HPACML_MAX_CNN_WIDTH.  On success writes the output image's rows, columns
+ * and channels (out_shape[3], may be NULL).  Returns what hpacml_cnn_create
+ * would return for the same arguments. */
+hpacml_status hpacml_cnn_validate(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                                  const hpacml_layer *layers, int32_t *out_shape);
+
+/* Creates a convolutional model for images of height x width x in_channels.
+ *   layers: [n_layers], read during the call only.
+ *   W[l], b[l]: HOST fp32 (CONV2D [out][in][kh][kw] and [out]; LINEAR
+ *   [out][rows*columns*channels of its input] and [out]; MAXPOOL2D: NULL).
+ *   compute: HPACML_F32.
+ * Weights are copied to library-owned device memory.  hpacml_infer with such a
+ * model either runs one fused kernel (convolution-only stacks of SAME, stride-1
+ * layers of at most 16 channels whose padding modes are all CIRCULAR or none
+ * CIRCULAR, on maps in the 32-bit form whose `from` targets do not meet the
+ * `to` targets), or a layer-by-layer path through a workspace of
+ * S * (largest layer tensor) * 3 floats that the model owns (allocated on first
+ * need, grown as needed, freed with the model).  That path reads every input
+ * before writing any output, so `from` targets may overlap `to` targets; calls
+ * that share a model must not overlap in time on different streams.  Errors
+ * as hpacml_cnn_validate, plus HPACML_E_NOMEM / HPACML_E_DEVICE. */
+hpacml_status hpacml_cnn_create(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                                const hpacml_layer *layers, const float *const *W, const float *const *b,
+                                int32_t compute, hpacml_model **out);
 
 /* Inference mode of a region (Sec. III-C `ml(infer)`, Sec. IV-B): for every
  * sweep point, gather through `in` (a TO map), run the model, write the outputs

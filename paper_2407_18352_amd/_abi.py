@@ -11,6 +11,9 @@ TO, FROM = 0, 1
 BND_NONE, BND_PERIODIC, BND_CLAMP = 0, 1, 2
 F32, BF16 = 0, 1
 ACT_IDENTITY, ACT_RELU = 0, 1
+LAYER_CONV2D, LAYER_MAXPOOL2D, LAYER_LINEAR = 0, 1, 2
+PAD_VALID, PAD_SAME = 0, 1
+PADMODE_ZEROS, PADMODE_CIRCULAR, PADMODE_REPLICATE = 0, 1, 2
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libhpacml.so")
 
@@ -34,6 +37,11 @@ class Sweep(C.Structure):
                 ("step", C.c_int64 * MAX_RANK)]
 
 
+class Layer(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("out_channels", C.c_int32), ("kernel", C.c_int32 * 2),
+                ("stride", C.c_int32 * 2), ("padding", C.c_int32), ("pad_mode", C.c_int32), ("act", C.c_int32)]
+
+
 # every symbol the header declares, with (restype, argtypes)
 _P = C.POINTER
 SIGNATURES = {
@@ -54,6 +62,9 @@ SIGNATURES = {
     "hpacml_collect_pair": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int64,
                                       C.c_void_p]),
     "hpacml_infer_variant": (C.c_char_p, [C.c_void_p, C.c_void_p, C.c_void_p]),
+    "hpacml_cnn_validate": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(C.c_int32)]),
+    "hpacml_cnn_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(_P(C.c_float)),
+                                    _P(_P(C.c_float)), C.c_int32, _P(C.c_void_p)]),
 }
 
 _lib = None

@@ -147,6 +147,68 @@ class Model:
             pass
 
 
+_KIND = {"conv": _abi.LAYER_CONV2D, "pool": _abi.LAYER_MAXPOOL2D, "linear": _abi.LAYER_LINEAR}
+_PADDING = {"valid": _abi.PAD_VALID, "same": _abi.PAD_SAME}
+_PAD_MODE = {"zeros": _abi.PADMODE_ZEROS, "circular": _abi.PADMODE_CIRCULAR, "replicate": _abi.PADMODE_REPLICATE}
+
+
+def _layers(spec):
+    """``hpacml_layer`` array from a convolutional model spec."""
+    Ls = spec["layers"]
+    arr = (_abi.Layer * len(Ls))()
+    for i, ly in enumerate(Ls):
+        a = arr[i]
+        a.kind = _KIND[ly["kind"]]
+        a.out_channels = int(ly.get("out", 0))
+        k = ly.get("kernel", (1, 1))
+        st = ly.get("stride", k if ly["kind"] == "pool" else (1, 1))
+        a.kernel[0], a.kernel[1] = int(k[0]), int(k[1])
+        a.stride[0], a.stride[1] = int(st[0]), int(st[1])
+        a.padding = _PADDING[ly.get("padding", "valid")]
+        a.pad_mode = _PAD_MODE[ly.get("mode", "zeros")]
+        a.act = int(ly.get("act", 0))
+    return arr
+
+
+def validate_cnn(spec):
+    """``hpacml_cnn_validate``: (status, output (rows, columns, channels))."""
+    H, W = spec["image"]
+    arr = _layers(spec)
+    shp = (C.c_int32 * 3)()
+    st = lib().hpacml_cnn_validate(int(spec["in_channels"]), int(H), int(W), len(spec["layers"]), arr, shp)
+    return st, tuple(shp)
+
+
+class CnnModel:
+    """A convolutional surrogate (convolution / max-pool / fully connected
+    layers on the composed tensor seen as images); spec as in
+    ``workloads.make_cnn``.  Weights are host fp32 arrays, copied into
+    library-owned device memory."""
+
+    def __init__(self, spec):
+        import numpy as np
+        Ls = spec["layers"]
+        L = len(Ls)
+        arr = _layers(spec)
+        self.W = [None if ly["kind"] == "pool" else np.ascontiguousarray(np.asarray(ly["W"], np.float32))
+                  for ly in Ls]
+        self.b = [None if ly["kind"] == "pool" else np.ascontiguousarray(np.asarray(ly["b"], np.float32))
+                  for ly in Ls]
+        null = C.POINTER(C.c_float)()
+        Wp = (C.POINTER(C.c_float) * L)(*[null if w is None else w.ctypes.data_as(C.POINTER(C.c_float))
+                                          for w in self.W])
+        bp = (C.POINTER(C.c_float) * L)(*[null if b is None else b.ctypes.data_as(C.POINTER(C.c_float))
+                                          for b in self.b])
+        H, W = spec["image"]
+        h = C.c_void_p()
+        check(lib().hpacml_cnn_create(int(spec["in_channels"]), int(H), int(W), L, arr, Wp, bp, _abi.F32,
+                                      C.byref(h)), "hpacml_cnn_create")
+        self.handle = h
+
+    close = Model.close
+    __del__ = Model.__del__
+
+
 def _stream(stream):
     if stream is None:
         import torch

@@ -10,6 +10,7 @@
 #include <vector>
 
 #include "hpacml.h"
+#include "cnn.hpp"
 #include "kernels.hpp"
 #include "plan.hpp"
 
@@ -47,6 +48,17 @@ struct hpacml_model_s {
     F32Packed f32{};
     uint16_t *bf16_frags = nullptr;  // packed fragments of the bf16 kernel
     BF16Packed bf16{};
+    // convolutional models
+    bool cnn = false;
+    CnnPlan cnnp;
+    float *cnn_buf = nullptr;        // the caller's layouts, every layer
+    std::vector<CnnLayerDev> cnn_layers;
+    bool cnn_fused = false;          // the fused kernel takes this stack
+    float *fused_buf = nullptr;      // its packed weights
+    CnnFused fused{};
+    std::mutex ws_mu;                // layer-by-layer workspace, grown on demand
+    float *ws = nullptr;
+    int64_t ws_floats = 0;
 };
 
 namespace {
@@ -133,10 +145,23 @@ hpacml_status check_infer(const hpacml_model *model, const hpacml_map *in, const
         return HPACML_E_INVAL;
     if (in->plan.dir != HPACML_TO || out->plan.dir != HPACML_FROM)
         return HPACML_E_INVAL;
-    if (in->plan.n_points != out->plan.n_points)
-        return HPACML_E_SHAPE;
-    if (in->plan.n_features != model->dims[0] || out->plan.n_features != model->dims[model->n_layers])
-        return HPACML_E_SHAPE;
+    if (model->cnn) {
+        // images: the last two sweep dimensions; leading ones number the images
+        const CnnPlan &c = model->cnnp;
+        const MapPlan &ip = in->plan;
+        if (ip.rank < 2 || ip.count[ip.rank - 2] != c.height || ip.count[ip.rank - 1] != c.width ||
+            ip.n_features != c.in_channels)
+            return HPACML_E_SHAPE;
+        const int64_t S = ip.n_points / ((int64_t)c.height * c.width);
+        const CnnShape &o = c.shape[c.n_layers];
+        if (out->plan.n_points != S * o.h * o.w || out->plan.n_features != o.c)
+            return HPACML_E_SHAPE;
+    } else {
+        if (in->plan.n_points != out->plan.n_points)
+            return HPACML_E_SHAPE;
+        if (in->plan.n_features != model->dims[0] || out->plan.n_features != model->dims[model->n_layers])
+            return HPACML_E_SHAPE;
+    }
     if (in->device != model->device || out->device != model->device || !same_device(model->device))
         return HPACML_E_INVAL;
     const Overlap ov = classify_overlap(in->plan, out->plan);
@@ -424,6 +449,9 @@ void hpacml_model_destroy(hpacml_model *m) {
     (void)hipFree(m->gen_buf);
     (void)hipFree(m->f32_img);
     (void)hipFree(m->bf16_frags);
+    (void)hipFree(m->cnn_buf);
+    (void)hipFree(m->fused_buf);
+    (void)hipFree(m->ws);
     delete m;
 }
 
@@ -527,6 +555,174 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
     }
 }
 
+hpacml_status hpacml_cnn_validate(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                                  const hpacml_layer *layers, int32_t *out_shape) {
+    CnnPlan p;
+    hpacml_status s = validate_cnn(in_channels, height, width, n_layers, layers, &p);
+    if (s == HPACML_OK && out_shape) {
+        out_shape[0] = p.shape[n_layers].h;
+        out_shape[1] = p.shape[n_layers].w;
+        out_shape[2] = p.shape[n_layers].c;
+    }
+    return s;
+}
+
+hpacml_status hpacml_cnn_create(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                                const hpacml_layer *layers, const float *const *W, const float *const *b,
+                                int32_t compute, hpacml_model **out) {
+    if (!out)
+        return HPACML_E_INVAL;
+    *out = nullptr;
+    CnnPlan p;
+    hpacml_status s = validate_cnn(in_channels, height, width, n_layers, layers, &p);
+    if (s != HPACML_OK)
+        return s;
+    if (compute != HPACML_F32)
+        return HPACML_E_UNSUPPORTED;
+    if (!W || !b)
+        return HPACML_E_INVAL;
+    for (int l = 0; l < n_layers; ++l)
+        if (layers[l].kind != HPACML_LAYER_MAXPOOL2D && (!W[l] || !b[l]))
+            return HPACML_E_INVAL;
+    hpacml_model *m = nullptr;
+    try {
+        m = new hpacml_model_s();
+        m->cnn = true;
+        m->n_layers = n_layers;
+        m->compute = compute;
+        if (hipGetDevice(&m->device) != hipSuccess) {
+            (void)hipGetLastError();
+            hpacml_model_destroy(m);
+            return HPACML_E_DEVICE;
+        }
+        // every layer's weights and biases in the caller's layouts
+        std::vector<float> host;
+        std::vector<size_t> woff(n_layers), boff(n_layers);
+        for (int l = 0; l < n_layers; ++l) {
+            const hpacml_layer &y = layers[l];
+            const CnnShape &si = p.shape[l], &so = p.shape[l + 1];
+            size_t nw = 0;
+            if (y.kind == HPACML_LAYER_CONV2D)
+                nw = (size_t)so.c * si.c * y.kernel[0] * y.kernel[1];
+            else if (y.kind == HPACML_LAYER_LINEAR)
+                nw = (size_t)so.c * si.h * si.w * si.c;
+            woff[l] = host.size();
+            if (nw)
+                host.insert(host.end(), W[l], W[l] + nw);
+            boff[l] = host.size();
+            if (y.kind != HPACML_LAYER_MAXPOOL2D)
+                host.insert(host.end(), b[l], b[l] + so.c);
+        }
+        if (host.empty())
+            host.push_back(0.f);   // a stack of pools only: no weights, a valid buffer all the same
+        s = upload(&m->cnn_buf, host.data(), host.size());
+        if (s == HPACML_OK && cnn_fused_supported(p)) {
+            std::vector<float> packed;
+            cnn_fused_pack(p, W, b, packed, &m->fused);
+            s = upload(&m->fused_buf, packed.data(), packed.size());
+            m->fused.wts = m->fused_buf;
+            m->cnn_fused = true;
+        }
+        if (s != HPACML_OK) {
+            hpacml_model_destroy(m);
+            return s;
+        }
+        for (int l = 0; l < n_layers; ++l) {
+            const hpacml_layer &y = layers[l];
+            CnnLayerDev d{};
+            d.kind = y.kind;
+            d.cin = p.shape[l].c;
+            d.cout = p.shape[l + 1].c;
+            d.kh = y.kind == HPACML_LAYER_LINEAR ? 1 : y.kernel[0];
+            d.kw = y.kind == HPACML_LAYER_LINEAR ? 1 : y.kernel[1];
+            d.sh = y.kind == HPACML_LAYER_LINEAR ? 1 : y.stride[0];
+            d.sw = y.kind == HPACML_LAYER_LINEAR ? 1 : y.stride[1];
+            d.same = y.kind == HPACML_LAYER_CONV2D && y.padding == HPACML_PAD_SAME;
+            d.mode = y.pad_mode;
+            d.act = y.act;
+            d.h = p.shape[l].h;
+            d.w = p.shape[l].w;
+            d.h2 = p.shape[l + 1].h;
+            d.w2 = p.shape[l + 1].w;
+            d.W = m->cnn_buf + woff[l];
+            d.b = m->cnn_buf + boff[l];
+            m->cnn_layers.push_back(d);
+        }
+        m->cnnp = std::move(p);
+        *out = m;
+        return HPACML_OK;
+    } catch (const std::bad_alloc &) {
+        hpacml_model_destroy(m);
+        return HPACML_E_NOMEM;
+    } catch (...) {
+        hpacml_model_destroy(m);
+        return HPACML_E_INVAL;
+    }
+}
+
+namespace {
+
+bool maps_disjoint(const MapPlan &a, const MapPlan &b) {
+    for (int i = 0; i < a.n_targets; ++i)
+        for (int j = 0; j < b.n_targets; ++j)
+            if (!disjoint_targets(a, i, b, j))
+                return false;
+    return true;
+}
+
+// The fused convolution kernel takes this call: 32-bit maps, outputs that
+// meet no input (its tiles read their neighbours' pixels), and a tile that
+// fits in LDS.
+bool cnn_use_fused(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+    return model->cnn_fused && in->t32 && out->t32 && maps_disjoint(in->plan, out->plan) &&
+           cnn_fused_tile_rows(model->fused, model->cnnp.height) > 0;
+}
+
+hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out, hipStream_t st) {
+    const CnnPlan &c = model->cnnp;
+    const int64_t S = in->plan.n_points / ((int64_t)c.height * c.width);
+    if (cnn_use_fused(model, in, out))
+        return hip_status(launch_cnn_fused(in->m32, out->m32, in->tab, out->tab, model->fused, (int32_t)S, c.height,
+                                           c.width, st));
+    // layer by layer: gather every input into the workspace first, so the
+    // outputs may overwrite inputs
+    hpacml_model *mm = const_cast<hpacml_model *>(model);
+    const int64_t per = S * c.max_elems;
+    float *a = nullptr, *b = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(mm->ws_mu);
+        if (mm->ws_floats < 2 * per) {
+            float *buf = nullptr;
+            hipError_t e = hipMalloc((void **)&buf, (size_t)(2 * per) * sizeof(float));
+            if (e != hipSuccess) {
+                (void)hipGetLastError();
+                return hip_status(e);
+            }
+            // the old workspace may still be in use by work queued on this stream
+            e = hipStreamSynchronize(st);
+            (void)hipFree(mm->ws);
+            mm->ws = buf;
+            mm->ws_floats = 2 * per;
+            if (e != hipSuccess)
+                return hip_status(e);
+        }
+        a = mm->ws;
+        b = mm->ws + per;
+    }
+    hpacml_status s = hpacml_collect(in, a, c.in_channels, st);
+    if (s != HPACML_OK)
+        return s;
+    for (int l = 0; l < c.n_layers; ++l) {
+        hipError_t e = launch_cnn_layer(model->cnn_layers[l], a, b, S, st);
+        if (e != hipSuccess)
+            return hip_status(e);
+        std::swap(a, b);
+    }
+    return hip_status(launch_scatter_record(out->dev, a, st));
+}
+
+}  // namespace
+
 namespace {
 
 // The snapshot record of a TO map ([points x features], row-major, at `buf`)
@@ -621,6 +817,8 @@ const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in
     bool snapshot = false;
     if (check_infer(model, in, out, &snapshot) != HPACML_OK)
         return nullptr;
+    if (model->cnn)
+        return cnn_use_fused(model, in, out) ? "cnn_fused_f32" : "cnn_layers_f32";
     if (!snapshot)
         return kernel_name(model, in->t32 && out->t32);
     return snapshot_name(kernel_name(model, snapshot_t32(in) && out->t32));
@@ -635,6 +833,8 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
     if (in->plan.n_points == 0)
         return HPACML_OK;
     hipStream_t st = (hipStream_t)stream;
+    if (model->cnn)
+        return cnn_infer(model, in, out, st);
     if (snapshot) {
         // the outputs may overwrite elements that other points still read:
         // every point's inputs go to the snapshot record first, and the model

@@ -1,0 +1,48 @@
+// Convolutional surrogates (the image-shaped model spaces of Table VI):
+// host plan, the layer-by-layer kernels and the fused convolution-stack
+// kernel.
+#pragma once
+
+#include <vector>
+
+#include "kernels.hpp"
+
+namespace hpacml {
+
+// ---- layer-by-layer path: one kernel per layer over S images ([S][h][w][c]
+// tensors in a workspace), then a scatter of the last one.
+struct CnnLayerDev {
+    int32_t kind, cin, cout, kh, kw, sh, sw, same, mode, act;
+    int32_t h, w, h2, w2;          // input and output image sizes
+    const float *W, *b;            // device, the caller's layouts
+};
+hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, hipStream_t stream);
+// src[p * F + g] -> feature g of point p of the (FROM) map
+hipError_t launch_scatter_record(const DevMap &m, const float *src, hipStream_t stream);
+
+// ---- fused path: a stack of SAME, stride-1 convolutions of at most 16
+// channels in one kernel (gather -> every layer in LDS -> scatter).
+constexpr int kCnnFusedMaxLayers = 4;
+constexpr int kCnnFusedMaxC = 16;
+struct CnnFusedLayer {
+    int32_t cin4, cout4;           // channel groups of 4 (zero padded)
+    int32_t kh, kw, top, left;     // window; padding rows / columns before
+    int32_t act;
+    int32_t mode;                  // padding mode of this layer's input
+    int32_t woff, boff;            // float offsets of the packed weights / biases
+};
+struct CnnFused {
+    int32_t n_layers = 0, c0 = 0, cout_last = 0, circular = 0;
+    CnnFusedLayer L[kCnnFusedMaxLayers]{};
+    const float *wts = nullptr;    // device: per layer [ky][kx][cin4*4][cout4*4], then bias [cout4*4]
+};
+bool cnn_fused_supported(const CnnPlan &p);
+// Packs the host weights; `out.wts` is left for the caller to set.
+void cnn_fused_pack(const CnnPlan &p, const float *const *W, const float *const *b, std::vector<float> &buf,
+                    CnnFused *out);
+// Rows per tile (64 columns) for this stack, or 0 when no tile fits in LDS.
+int cnn_fused_tile_rows(const CnnFused &f, int32_t H);
+hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                            const CnnFused &f, int32_t S, int32_t H, int32_t W, hipStream_t stream);
+
+}  // namespace hpacml

@@ -299,3 +299,75 @@ Overlap classify_overlap(const MapPlan &in, const MapPlan &out) {
 }
 
 }  // namespace hpacml
+
+// ---- convolutional models --------------------------------------------------
+
+namespace hpacml {
+
+hpacml_status validate_cnn(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                           const hpacml_layer *layers, CnnPlan *out) {
+    if (!layers || n_layers < 1 || n_layers > HPACML_MAX_LAYERS)
+        return HPACML_E_INVAL;
+    if (in_channels < 1 || in_channels > HPACML_MAX_FEATURES || height < 1 || width < 1)
+        return HPACML_E_INVAL;
+    CnnPlan p;
+    p.in_channels = in_channels;
+    p.height = height;
+    p.width = width;
+    p.n_layers = n_layers;
+    p.layers.assign(layers, layers + n_layers);
+    int64_t h = height, w = width, c = in_channels;
+    bool flat = false;
+    p.shape.push_back({(int32_t)h, (int32_t)w, (int32_t)c});
+    for (int l = 0; l < n_layers; ++l) {
+        const hpacml_layer &y = layers[l];
+        if (y.act != HPACML_ACT_IDENTITY && y.act != HPACML_ACT_RELU)
+            return HPACML_E_INVAL;
+        if (y.kind == HPACML_LAYER_LINEAR) {
+            if (h * w * c > HPACML_MAX_CNN_WIDTH)
+                return HPACML_E_UNSUPPORTED;
+            c = y.out_channels;
+            h = w = 1;
+            flat = true;
+        } else if (y.kind == HPACML_LAYER_CONV2D || y.kind == HPACML_LAYER_MAXPOOL2D) {
+            if (flat)
+                return HPACML_E_INVAL;
+            if (y.kernel[0] < 1 || y.kernel[1] < 1 || y.stride[0] < 1 || y.stride[1] < 1)
+                return HPACML_E_INVAL;
+            const bool same = y.kind == HPACML_LAYER_CONV2D && y.padding == HPACML_PAD_SAME;
+            if (y.kind == HPACML_LAYER_CONV2D) {
+                if (y.padding != HPACML_PAD_SAME && y.padding != HPACML_PAD_VALID)
+                    return HPACML_E_INVAL;
+                if (same && (y.pad_mode < HPACML_PADMODE_ZEROS || y.pad_mode > HPACML_PADMODE_REPLICATE))
+                    return HPACML_E_INVAL;
+                if (y.kernel[0] > 64 || y.kernel[1] > 64)
+                    return HPACML_E_UNSUPPORTED;
+            }
+            if (same) {
+                if (y.stride[0] != 1 || y.stride[1] != 1)
+                    return HPACML_E_INVAL;
+            } else {
+                if (y.kernel[0] > h || y.kernel[1] > w)
+                    return HPACML_E_SHAPE;
+                h = (h - y.kernel[0]) / y.stride[0] + 1;
+                w = (w - y.kernel[1]) / y.stride[1] + 1;
+            }
+            if (y.kind == HPACML_LAYER_CONV2D)
+                c = y.out_channels;
+        } else {
+            return HPACML_E_INVAL;
+        }
+        if (c < 1)
+            return HPACML_E_INVAL;
+        if (c > HPACML_MAX_CNN_WIDTH)
+            return HPACML_E_UNSUPPORTED;
+        p.shape.push_back({(int32_t)h, (int32_t)w, (int32_t)c});
+    }
+    for (const CnnShape &s : p.shape)
+        p.max_elems = std::max(p.max_elems, (int64_t)s.h * s.w * s.c);
+    if (out)
+        *out = std::move(p);
+    return HPACML_OK;
+}
+
+}  // namespace hpacml

@@ -72,4 +72,21 @@ Overlap classify_overlap(const MapPlan &in, const MapPlan &out);
 // True when two targets provably address disjoint elements.
 bool disjoint_targets(const MapPlan &a, int ta, const MapPlan &b, int tb);
 
+// ---- convolutional models
+
+// Image shape (rows, columns, channels) at one point of the stack.
+struct CnnShape {
+    int32_t h, w, c;
+};
+
+// A validated convolutional model description (no device state).
+struct CnnPlan {
+    int32_t in_channels = 0, height = 0, width = 0, n_layers = 0;
+    std::vector<hpacml_layer> layers;
+    std::vector<CnnShape> shape;   // [n_layers + 1]: input of layer l; [n_layers] = output
+    int64_t max_elems = 0;         // largest h * w * c over `shape` (one image)
+};
+hpacml_status validate_cnn(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                           const hpacml_layer *layers, CnnPlan *out);
+
 }  // namespace hpacml

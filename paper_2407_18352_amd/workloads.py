@@ -278,3 +278,108 @@ def edge_rows_2d(ny: int, nx: int) -> np.ndarray:
         for a in range(ny):
             cells.add(a * nx + c)
     return np.asarray(sorted(cells), np.int64)
+
+
+# ---- convolutional surrogates (Table VI model spaces) ----------------------
+# * ``weather_cnn``  MiniWeather-like: 4 periodic state fields on an ny x nx
+#   grid (sums of sinusoids, as ``stencil2d``); conv 5x5 4 -> 8 (circular,
+#   ReLU), conv 3x3 8 -> 4 (circular); kernel sizes and channels from the
+#   middle of the searched ranges (layer-1 kernel 2-8, 4-8 channels, layer-2
+#   kernel 0-6).  Full size 2048 x 2048, the 2-D stencil's grid.
+# * ``particle_cnn`` ParticleFilter-like: S video frames of H x W pixels (a
+#   bright disc moving across a noisy background), conv 4x4 step 4 1 -> 8
+#   (valid, ReLU), max-pool 2x2, fully connected 2048 -> 64 (ReLU) -> 2 (the
+#   object's location).  Full size 1024 frames of 128 x 128.
+CNN_NAMES = ("weather_cnn", "particle_cnn")
+CNN_FULL = {"weather_cnn": (2048, 2048), "particle_cnn": (1024, 128, 128)}
+CNN_SMALL = {"weather_cnn": (37, 150), "particle_cnn": (3, 128, 128)}
+
+
+def conv_layer(cfg, k, cin, cout, kernel, padding="same", mode="circular", stride=(1, 1), act=RELU) -> dict:
+    """He-normal weights N(0, 2/fan_in), biases U(-1/sqrt(fan_in), 1/sqrt(fan_in))."""
+    fan = cin * kernel[0] * kernel[1]
+    W = (rng(cfg, k).standard_normal((cout, cin) + tuple(kernel)) * math.sqrt(2.0 / fan)).astype(np.float32)
+    b = rng(cfg, k + 1).uniform(-1 / math.sqrt(fan), 1 / math.sqrt(fan), cout).astype(np.float32)
+    return {"kind": "conv", "out": cout, "kernel": tuple(kernel), "stride": tuple(stride), "padding": padding,
+            "mode": mode, "act": act, "W": W, "b": b}
+
+
+def linear_layer(cfg, k, fin, fout, act=RELU) -> dict:
+    W = (rng(cfg, k).standard_normal((fout, fin)) * math.sqrt(2.0 / fin)).astype(np.float32)
+    b = rng(cfg, k + 1).uniform(-1 / math.sqrt(fin), 1 / math.sqrt(fin), fout).astype(np.float32)
+    return {"kind": "linear", "out": fout, "act": act, "W": W, "b": b}
+
+
+def video_frames(cfg: int, k: int, S: int, H: int, W: int) -> np.ndarray:
+    """S frames: background 0.4 + N(0, 0.05) noise and a disc of radius H/16
+    and value 0.9 moving on a straight line across the frame."""
+    g = rng(cfg, k)
+    f = (0.4 + g.normal(0.0, 0.05, (S, H, W))).astype(np.float32)
+    y0, x0 = g.uniform(0.2, 0.8, 2) * (H, W)
+    vy, vx = g.uniform(-1.0, 1.0, 2)
+    r = H / 16
+    yy = np.arange(H)[:, None]
+    xx = np.arange(W)[None, :]
+    for s in range(S):
+        cy, cx = (y0 + vy * s) % H, (x0 + vx * s) % W
+        f[s][(yy - cy) ** 2 + (xx - cx) ** 2 <= r * r] = 0.9
+    return f
+
+
+def make_cnn(name: str, size=None) -> Workload:
+    """A convolutional workload; ``model`` is ``{"kind": "cnn", "in_channels",
+    "image": (rows, columns), "layers": [...]}`` (the layer dicts of
+    ``conv_layer`` / ``linear_layer`` and ``{"kind": "pool", "kernel"}``)."""
+    cfg = 10 + CNN_NAMES.index(name)
+    if size is None or size == "full":
+        size = CNN_FULL[name]
+    elif size == "small":
+        size = CNN_SMALL[name]
+    if name == "weather_cnn":
+        ny, nx = size
+        inputs = [sinusoid_field(cfg, k, ny, nx) for k in range(4)]
+        layers = [conv_layer(cfg, 100, 4, 8, (5, 5)), conv_layer(cfg, 110, 8, 4, (3, 3), act=IDENTITY)]
+        model = {"kind": "cnn", "in_channels": 4, "image": (ny, nx), "layers": layers, "compute": "f32"}
+        ins, outs = point2d_spec(ny, nx), point2d_spec(ny, nx)
+        outputs = [sentinel_like((ny, nx)) for _ in range(4)]
+        dims = [4, 4]
+    elif name == "particle_cnn":
+        S, H, W = size
+        inputs = [video_frames(cfg, 0, S, H, W)]
+        c1 = conv_layer(cfg, 100, 1, 8, (4, 4), padding="valid", mode="zeros", stride=(4, 4))
+        h, w = (H - 4) // 4 + 1, (W - 4) // 4 + 1
+        h, w = (h - 2) // 2 + 1, (w - 2) // 2 + 1
+        layers = [c1, {"kind": "pool", "kernel": (2, 2), "act": IDENTITY},
+                  linear_layer(cfg, 110, h * w * 8, 64), linear_layer(cfg, 120, 64, 2, act=IDENTITY)]
+        model = {"kind": "cnn", "in_channels": 1, "image": (H, W), "layers": layers, "compute": "f32"}
+        ins = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+               "bnd": [NONE] * 3}
+        outs = pointwise_spec(S)
+        outputs = [sentinel_like((S,)) for _ in range(2)]
+        dims = [1, 2]
+    else:
+        raise KeyError(name)
+    return Workload(name, cfg, "f32", dims, ins, outs, inputs, outputs, model)
+
+
+def cnn_flops_per_image(model) -> int:
+    """Multiply-adds x 2 of one image through the stack (max-pool: none)."""
+    H, W = model["image"]
+    h, w, c = H, W, model["in_channels"]
+    total = 0
+    for ly in model["layers"]:
+        if ly["kind"] == "conv":
+            kh, kw = ly["kernel"]
+            if ly.get("padding", "valid") == "valid":
+                sh, sw = ly.get("stride", (1, 1))
+                h, w = (h - kh) // sh + 1, (w - kw) // sw + 1
+            total += 2 * h * w * ly["out"] * c * kh * kw
+            c = ly["out"]
+        elif ly["kind"] == "pool":
+            kh, kw = ly["kernel"]
+            sh, sw = ly.get("stride", ly["kernel"])
+            h, w = (h - kh) // sh + 1, (w - kw) // sw + 1
+        else:
+            total += 2 * h * w * c * ly["out"]
+            h, w, c = 1, 1, ly["out"]
+    return total

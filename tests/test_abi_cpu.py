@@ -25,7 +25,7 @@ def header_functions():
 
 def test_library_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 13
+    assert len(names) == 15
     L = C.CDLL(_abi.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -37,7 +37,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_version_and_status_strings():
     L = _abi.lib()
-    assert L.hpacml_abi_version() == 1
+    assert L.hpacml_abi_version() == 2
     for s in range(8):
         assert L.hpacml_status_string(s)
     assert L.hpacml_status_string(0) == b"ok"
@@ -194,3 +194,28 @@ def test_model_create_rejects_before_device_work():
     assert L.hpacml_infer_variant(None, None, None) is None
     L.hpacml_map_destroy(None)
     L.hpacml_model_destroy(None)
+
+
+def test_cnn_validate_shapes_and_errors():
+    """Convolutional model descriptions: output shapes of the two workload
+    stacks, and each rejected form reported without a device."""
+    for name, want in [("weather_cnn", (2048, 2048, 4)), ("particle_cnn", (1, 1, 2))]:
+        w = wl.make_cnn(name, "full") if name == "particle_cnn" else wl.make_cnn(name, (2048, 2048))
+        st, shp = api.validate_cnn(w.model)
+        assert st == _abi.OK and shp == want, name
+    conv = wl.conv_layer(1, 0, 4, 8, (3, 3))
+    base = {"kind": "cnn", "in_channels": 4, "image": (16, 16), "layers": [conv]}
+    assert api.validate_cnn(base)[0] == _abi.OK
+    # SAME with a step
+    assert api.validate_cnn(dict(base, layers=[dict(conv, stride=(1, 2))]))[0] == _abi.E_INVAL
+    # VALID window larger than the image
+    assert api.validate_cnn(dict(base, layers=[dict(conv, padding="valid", kernel=(17, 3))]))[0] == _abi.E_SHAPE
+    # a convolution after a fully connected layer
+    lin = wl.linear_layer(1, 0, 16 * 16 * 8, 5)
+    assert api.validate_cnn(dict(base, layers=[conv, lin, conv]))[0] == _abi.E_INVAL
+    # no layers, bad channels, bad image
+    assert api.validate_cnn(dict(base, layers=[]))[0] == _abi.E_INVAL
+    assert api.validate_cnn(dict(base, in_channels=0))[0] == _abi.E_INVAL
+    assert api.validate_cnn(dict(base, image=(0, 4)))[0] == _abi.E_INVAL
+    # zero output channels
+    assert api.validate_cnn(dict(base, layers=[dict(conv, out=0)]))[0] == _abi.E_INVAL

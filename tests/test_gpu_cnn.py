@@ -1,0 +1,243 @@
+"""GPU parity of the convolutional surrogates (called through the C ABI)
+against the oracle: fp32 outputs within |g - o| <= 1e-5 * max(|o|, s)
+(s = RMS of the oracle's output column), no NaN where the oracle has none,
+untouched elements keep their sentinel bits."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2407_18352_amd import _abi, api
+from paper_2407_18352_amd import workloads as wl
+from gpu_util import RTOL, assert_close, require_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _run(w, fields_out=None):
+    """The region on the GPU; returns (outputs as numpy, variant)."""
+    import torch
+    ins = to_dev(w.inputs)
+    outs = ins if fields_out == "inplace" else to_dev(w.outputs)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.FROM)
+    m = api.CnnModel(w.model)
+    var = api.variant(m, mi, mo)
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    return [t.cpu().numpy() for t in outs], var
+
+
+def _expected(w, inplace=False):
+    src = [a.copy() for a in w.inputs]
+    dst = src if inplace else [a.copy() for a in w.outputs]
+    oracle.infer(w.in_spec, src, w.out_spec, dst, w.model)
+    return dst
+
+
+def _compare(got, want, what, rtol=RTOL["f32"]):
+    g = np.stack([a.reshape(-1) for a in got], 1)
+    e = np.stack([a.reshape(-1) for a in want], 1)
+    return assert_close(g, e, rtol, what)
+
+
+def _rtol_for(model):
+    """The fp32 bar holds for the searched stacks (at most two convolutions,
+    sums of at most 256 terms: 8x8 windows over 4 channels, 6x6 over 8).
+    Beyond that space it widens by sqrt(n / 256) for n-term sums and by L / 2
+    for L layers: rounding errors of an n-term fp32 sum grow like sqrt(n),
+    and each layer passes the earlier layers' errors on."""
+    n, L = 1, 0
+    c = model["in_channels"]
+    for ly in model["layers"]:
+        if ly["kind"] == "conv":
+            n = max(n, c * ly["kernel"][0] * ly["kernel"][1])
+            c = ly["out"]
+            L += 1
+    return RTOL["f32"] * max(1.0, (n / 256) ** 0.5) * max(1.0, L / 2)
+
+
+@pytest.mark.parametrize("name, want", [("weather_cnn", "cnn_fused_f32"), ("particle_cnn", "cnn_layers_f32")])
+def test_cnn_small(name, want):
+    w = wl.make_cnn(name, "small")
+    got, var = _run(w)
+    assert var == want
+    worst, norm = _compare(got, _expected(w), "%s via %s" % (name, var))
+    print("%s [%s]: worst scaled %.3e, normwise %.3e" % (name, var, worst, norm))
+
+
+def _random_stack(g, cin, n_layers, modes, max_c=16, max_k=8):
+    layers, c = [], cin
+    for l in range(n_layers):
+        cout = int(g.integers(1, max_c + 1))
+        k = (int(g.integers(1, max_k + 1)), int(g.integers(1, max_k + 1)))
+        layers.append(wl.conv_layer(int(g.integers(1 << 20)), 0, c, cout, k, mode=modes[l],
+                                    act=int(g.integers(0, 2))))
+        c = cout
+    return layers, c
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_fused_random_stacks(case):
+    """Random SAME stacks (1-4 layers, windows 1-8 incl. even, 1-16 channels,
+    every padding-mode family) on ragged images, one or several images."""
+    g = np.random.default_rng(1000 + case)
+    family = ["circular", "zeros", "replicate", "mixed"][case % 4]
+    n_layers = 1 + case % 4
+    if family == "mixed":
+        modes = [["zeros", "replicate"][int(g.integers(0, 2))] for _ in range(n_layers)]
+    else:
+        modes = [family] * n_layers
+    cin = int(g.integers(1, 17))
+    S = 1 + case % 3
+    H, W = [(1, 1), (2, 3), (5, 70), (33, 65), (40, 130), (3, 200)][case % 6]
+    layers, cout = _random_stack(g, cin, n_layers, modes)
+    model = {"kind": "cnn", "in_channels": cin, "image": (H, W), "layers": layers}
+    inputs = [g.standard_normal((S, H, W)).astype(np.float32) for _ in range(cin)]
+    spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+            "bnd": [0, 0, 0]}
+    outputs = [wl.sentinel_like((S, H, W)) for _ in range(cout)]
+    w = wl.Workload("random", 0, "f32", [cin, cout], spec, spec, inputs, outputs, model)
+    got, var = _run(w)
+    assert var == "cnn_fused_f32", var
+    _compare(got, _expected(w), "case %d (%s, %d layers, %dx%dx%d)" % (case, family, n_layers, S, H, W),
+             _rtol_for(model))
+
+
+@pytest.mark.parametrize("case", range(4))
+def test_layered_path_stacks(case):
+    """Stacks only the layer-by-layer path takes: circular mixed with other
+    modes, valid / strided convolutions, pools and fully connected layers,
+    more than 16 channels."""
+    g = np.random.default_rng(2000 + case)
+    S, H, W, cin = 2, 19, 23, 3
+    if case == 0:
+        layers = [wl.conv_layer(1, 0, cin, 5, (3, 3), mode="circular"), wl.conv_layer(2, 0, 5, 4, (4, 2), mode="zeros")]
+    elif case == 1:
+        layers = [wl.conv_layer(3, 0, cin, 20, (3, 3), mode="replicate"),
+                  wl.conv_layer(4, 0, 20, 2, (1, 1), act=0)]
+    elif case == 2:
+        layers = [wl.conv_layer(5, 0, cin, 6, (5, 3), padding="valid", stride=(2, 3)),
+                  {"kind": "pool", "kernel": (2, 2), "stride": (1, 2)}]
+    else:
+        layers = [wl.conv_layer(6, 0, cin, 4, (3, 3), padding="valid", mode="zeros", stride=(2, 2)),
+                  {"kind": "pool", "kernel": (3, 3)}]
+        h, w_, c = oracle.cnn_shapes({"kind": "cnn", "in_channels": cin, "image": (H, W), "layers": layers})[-1]
+        layers += [wl.linear_layer(7, 0, h * w_ * c, 9), wl.linear_layer(8, 0, 9, 3, act=0)]
+    model = {"kind": "cnn", "in_channels": cin, "image": (H, W), "layers": layers}
+    h2, w2, c2 = oracle.cnn_shapes(model)[-1]
+    inputs = [g.standard_normal((S, H, W)).astype(np.float32) for _ in range(cin)]
+    ins = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+           "bnd": [0, 0, 0]}
+    outs = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, h2, w2), (1, 1, 1)),
+            "bnd": [0, 0, 0]}
+    outputs = [wl.sentinel_like((S, h2, w2)) for _ in range(c2)]
+    w = wl.Workload("layered", 0, "f32", [cin, c2], ins, outs, inputs, outputs, model)
+    got, var = _run(w)
+    assert var == "cnn_layers_f32", var
+    _compare(got, _expected(w), "layered case %d" % case)
+
+
+def test_window_map_channels_and_strided_views():
+    """Channels from a 3x3 periodic window map (36 channels: layer by layer)
+    and from column views of one array of structures (fused)."""
+    import torch
+    g = np.random.default_rng(77)
+    ny, nx = 21, 67
+    fields = [wl.sinusoid_field(3, k, ny, nx) for k in range(4)]
+    model = {"kind": "cnn", "in_channels": 36, "image": (ny, nx),
+             "layers": [wl.conv_layer(1, 0, 36, 4, (3, 3), mode="replicate", act=0)]}
+    outputs = [wl.sentinel_like((ny, nx)) for _ in range(4)]
+    w = wl.Workload("window", 0, "f32", [36, 4], wl.window2d_spec(ny, nx), wl.point2d_spec(ny, nx), fields,
+                    outputs, model)
+    got, var = _run(w)
+    assert var == "cnn_layers_f32"
+    _compare(got, _expected(w), "window channels")
+    # array of structures [ny][nx][4]: four strided column views
+    aos = np.stack(fields, -1).copy()
+    dev = torch.from_numpy(aos).cuda()
+    views = [dev[:, :, k] for k in range(4)]
+    m4 = {"kind": "cnn", "in_channels": 4, "image": (ny, nx),
+          "layers": [wl.conv_layer(2, 0, 4, 7, (4, 4), mode="circular"), wl.conv_layer(3, 0, 7, 2, (3, 5),
+                                                                                       mode="circular", act=0)]}
+    outs = to_dev([wl.sentinel_like((ny, nx)) for _ in range(2)])
+    mi = api.Map(wl.point2d_spec(ny, nx), views, _abi.TO)
+    mo = api.Map(wl.point2d_spec(ny, nx), outs, _abi.FROM)
+    m = api.CnnModel(m4)
+    assert api.variant(m, mi, mo) == "cnn_fused_f32"
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    exp = [wl.sentinel_like((ny, nx)) for _ in range(2)]
+    oracle.infer(wl.point2d_spec(ny, nx), fields, wl.point2d_spec(ny, nx), exp, m4)
+    _compare([o.cpu().numpy() for o in outs], exp, "array of structures")
+
+
+def test_inplace_update_reads_every_input_first():
+    """A MiniWeather-like step written back into its own fields: the fused
+    tiles would read pixels other tiles have overwritten, so the layer-by-
+    layer path (every input gathered first) runs, and matches the oracle's
+    region on the same arrays."""
+    w = wl.make_cnn("weather_cnn", (29, 70))
+    got, var = _run(w, fields_out="inplace")
+    assert var == "cnn_layers_f32"
+    _compare(got, _expected(w, inplace=True), "in place")
+
+
+def test_pool_nan_propagates_and_relu_clears_nan():
+    g = np.random.default_rng(9)
+    S, H, W = 2, 8, 10
+    img = g.standard_normal((S, H, W)).astype(np.float32)
+    img[0, 3, 4] = np.nan
+    img[1, 0, 9] = np.nan
+    spec3 = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+             "bnd": [0, 0, 0]}
+    pool = {"kind": "cnn", "in_channels": 1, "image": (H, W), "layers": [{"kind": "pool", "kernel": (2, 2)}]}
+    out_spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, 4, 5), (1, 1, 1)),
+                "bnd": [0, 0, 0]}
+    w = wl.Workload("pool", 0, "f32", [1, 1], spec3, out_spec, [img], [wl.sentinel_like((S, 4, 5))], pool)
+    got, _ = _run(w)
+    exp = _expected(w)
+    assert np.array_equal(np.isnan(got[0]), np.isnan(exp[0])) and np.isnan(got[0]).sum() == 2
+    assert np.array_equal(got[0][~np.isnan(got[0])], exp[0][~np.isnan(exp[0])])
+    # a NaN pixel through a ReLU convolution: 0 where the oracle has 0
+    conv = {"kind": "cnn", "in_channels": 1, "image": (H, W),
+            "layers": [wl.conv_layer(4, 0, 1, 3, (3, 3), mode="zeros", act=1)]}
+    outs3 = [wl.sentinel_like((S, H, W)) for _ in range(3)]
+    w2 = wl.Workload("nan", 0, "f32", [1, 3], spec3, spec3, [img], outs3, conv)
+    got2, var2 = _run(w2)
+    assert var2 == "cnn_fused_f32"
+    _compare(got2, _expected(w2), "NaN through ReLU conv")
+
+
+def test_cnn_errors():
+    import torch
+    w = wl.make_cnn("weather_cnn", (16, 64))
+    ins, outs = to_dev(w.inputs), to_dev(w.outputs)
+    m = api.CnnModel(w.model)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    # image size differs from the model's
+    small = api.Map(wl.point2d_spec(16, 63), [x[:, :63] for x in outs], _abi.FROM)
+    mi63 = api.Map(wl.point2d_spec(16, 63), [x[:, :63] for x in ins], _abi.TO)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.infer(m, mi63, small)
+    assert e.value.status == _abi.E_SHAPE
+    # output feature count differs from the last layer's channels
+    mo3 = api.Map(w.out_spec, outs[:3], _abi.FROM)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.infer(m, mi, mo3)
+    assert e.value.status == _abi.E_SHAPE
+    # two outputs that can write one element
+    race = api.Map(w.out_spec, [outs[0], outs[0], outs[1], outs[2]], _abi.FROM)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.infer(m, mi, race)
+    assert e.value.status == _abi.E_ALIAS
+    # descriptions
+    bad = dict(w.model, layers=[dict(w.model["layers"][0], stride=(2, 1))])
+    assert api.validate_cnn(bad)[0] == _abi.E_INVAL
+    st, shp = api.validate_cnn(w.model)
+    assert st == _abi.OK and shp == (16, 64, 4)
+    torch.cuda.synchronize()
