@@ -27,6 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK = {"f32": 157.3e12, "bf16": 2.5e15}   # dense MFMA peaks of MI355X, flop/s
+VALU_F32_PEAK = 157.3e12                   # published fp32 vector peak (packed FMA; see the design notes)
 HBM_PEAK = 8.0e12                          # bytes/s
 
 DESCRIPTION = {
@@ -39,6 +40,10 @@ DESCRIPTION = {
              "activations with fp32 accumulate, 1 output",
     "stencil3d": "3-D stencil: 512^3 grid x 5 fp32 fields, periodic 7-point window (35 features), "
                  "MLP 35-512-512-5 ReLU, bf16 with fp32 accumulate, 5 outputs per cell",
+    "weather_cnn": "convolutional 2-D step: 2048x2048 grid x 4 fp32 fields, conv 5x5 4->8 circular ReLU, "
+                   "conv 3x3 8->4 circular, fp32, 4 outputs per cell",
+    "particle_cnn": "convolutional frame estimate: 1024 frames of 128x128 fp32 pixels, conv 4x4/4 1->8 ReLU, "
+                    "max-pool 2x2, FC 2048->64 ReLU, FC 64->2, fp32, 2 outputs per frame",
 }
 
 
@@ -47,6 +52,7 @@ KERNEL_SOURCES = {
     "mlp_f32": ["mlp_f32.hip", "device.hpp", "kernels.hpp"],
     "mlp_bf16": ["mlp_bf16.hip", "device.hpp", "kernels.hpp"],
     "mlp_generic": ["mlp_generic.hip", "device.hpp", "kernels.hpp"],
+    "cnn_": ["cnn.hip", "cnn.hpp", "device.hpp", "kernels.hpp"],
 }
 
 
@@ -102,7 +108,8 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     t0 = time.time()
-    w = wl.make(args.workload)
+    is_cnn = args.workload in wl.CNN_NAMES
+    w = wl.make_cnn(args.workload) if is_cnn else wl.make(args.workload)
     print("[bench] workload %s generated in %.1fs" % (args.workload, time.time() - t0), file=sys.stderr, flush=True)
 
     ins = [torch.from_numpy(a).cuda() for a in w.inputs]
@@ -110,11 +117,11 @@ def main():
     mi = api.Map(w.in_spec, ins, _abi.TO)
     mo = api.Map(w.out_spec, outs, _abi.FROM)
     mo_rec = api.Map(w.out_spec, outs, _abi.TO)        # the outputs as a recorded map
-    model = api.Model(w.model)
+    model = api.CnnModel(w.model) if is_cnn else api.Model(w.model)
     variant = api.variant(model, mi, mo)
-    B, Fi, Fo = mi.n_points, mi.n_features, mo.n_features
+    B, Fi, Fo, Bo = mi.n_points, mi.n_features, mo.n_features, mo.n_points
     rec_in = torch.empty((B, Fi), device="cuda")
-    rec_out = torch.empty((B, Fo), device="cuda")
+    rec_out = torch.empty((Bo, Fo), device="cuda")
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
@@ -154,13 +161,18 @@ def main():
     ms_step = total_ms / args.steps
     infer_avg = float(np.mean(infer_ms))
 
-    flops_pt = w.flops_per_point
-    achieved = flops_pt * B / (infer_avg * 1e-3)
-    peak = PEAK[w.compute]
+    if is_cnn:
+        H, W = w.model["image"]
+        flop_launch = wl.cnn_flops_per_image(w.model) * (B // (H * W))
+        peak, bound = VALU_F32_PEAK, "alu"
+    else:
+        flop_launch = w.flops_per_point * B
+        peak, bound = PEAK[w.compute], "mfma"
+    achieved = flop_launch / (infer_avg * 1e-3)
     traffic = recorded_traffic(variant, args.workload)
     # collect: every element of the mapped arrays read once, every record
     # word written once (in and out records)
-    collect_bytes = (sum(a.nbytes for a in w.inputs) + 4 * B * Fi) + (sum(a.nbytes for a in w.outputs) + 4 * B * Fo)
+    collect_bytes = (sum(a.nbytes for a in w.inputs) + 4 * B * Fi) + (sum(a.nbytes for a in w.outputs) + 4 * Bo * Fo)
     collect_avg = float(np.mean(collect_ms))
     collect_traffic = recorded_traffic("collect", args.workload)
     result = {
@@ -177,13 +189,14 @@ def main():
         "dtype": w.compute,
         "data": "synthetic (seeded generators; random-init He-normal weights)",
         "config": {"workload": DESCRIPTION[args.workload], "points": B, "features_in": Fi,
-                   "features_out": Fo},
-        "roofline": {"bound": "mfma", "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
+                   "features_out": Fo, "output_points": Bo},
+        "roofline": {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic["bytes"] if traffic else None,
                      "traffic_source": traffic["source"] if traffic else None,
-                     "algorithmic_hbm_bytes_per_launch": w.hbm_bytes_per_point * B,
+                     "algorithmic_hbm_bytes_per_launch": sum(a.nbytes for a in w.inputs) + sum(
+                         a.nbytes for a in w.outputs),
                      "kernel": variant, "kernel_avg_ms": infer_avg,
-                     "algorithmic_flop_per_launch": flops_pt * B},
+                     "algorithmic_flop_per_launch": flop_launch},
         "infer_points_per_s": B / (infer_avg * 1e-3),
         "infer_ms": {"mean": infer_avg, "median": float(np.median(infer_ms)), "min": float(np.min(infer_ms))},
         "collect_roofline": {"bound": "hbm", "achieved": collect_bytes / (collect_avg * 1e-3) / 1e9,
@@ -196,7 +209,34 @@ def main():
         "wall_s_timed": wall,
     }
 
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and is_cnn:
+        import oracle
+        # bounded sample: whole images (the oracle's unit), as many as fit the
+        # CPU-time target, repeated until it is reached
+        H, W = w.model["image"]
+        S = B // (H * W)
+        c0 = time.perf_counter()
+        X1 = oracle.gather(dict(w.in_spec, sweep=_first_images(w.in_spec, 1)), w.inputs)
+        Y1 = oracle.cnn(w.model, X1)
+        per_img = time.perf_counter() - c0
+        n_img = int(min(S, max(1, args.cpu_seconds / max(per_img, 1e-9))))
+        X = oracle.gather(dict(w.in_spec, sweep=_first_images(w.in_spec, n_img)), w.inputs)
+        reps, cpu_s = 0, 0.0
+        while reps == 0 or cpu_s < args.cpu_seconds:
+            c0 = time.perf_counter()
+            Y = oracle.cnn(w.model, X)
+            cpu_s += time.perf_counter() - c0
+            reps += 1
+        n_out = Y.shape[0]
+        got = np.stack([o.cpu().numpy().reshape(-1)[:n_out] for o in outs], 1).astype(np.float64)
+        s = np.sqrt(np.mean(Y.astype(np.float64) ** 2, axis=0, keepdims=True))
+        worst = float(np.max(np.abs(got - Y) / np.maximum(np.abs(Y), s)))
+        result["cpu_baseline"] = {"value": reps * n_img * H * W / cpu_s, "unit": "points/s",
+                                  "cores": oracle.num_threads(), "kind": "oracle",
+                                  "sample": "the first %d of %d images x %d passes, gather + convolutional model "
+                                            "in fp64, %.1fs" % (n_img, S, reps, cpu_s)}
+        result["parity_on_cpu_sample"] = {"worst_scaled_error": worst, "rtol": 1e-5}
+    elif not args.no_cpu_baseline:
         import oracle
         # bounded sample: as many seeded rows as fit the CPU-time target
         # (estimated from a short calibration run); when the whole batch takes
@@ -223,6 +263,15 @@ def main():
         result["parity_on_cpu_sample"] = {"worst_scaled_error": worst, "rtol": 1e-5 if w.compute == "f32" else 2e-2}
 
     print(json.dumps(result), flush=True)
+
+
+def _first_images(spec, n):
+    """The sweep of `spec` cut to its first n images (leading sweep dimension;
+    a rank-2 sweep is one image)."""
+    start, stop, step = (list(v) for v in spec["sweep"])
+    if spec["rank"] > 2:
+        stop[0] = min(stop[0], start[0] + n * step[0])
+    return tuple(start), tuple(stop), tuple(step)
 
 
 if __name__ == "__main__":

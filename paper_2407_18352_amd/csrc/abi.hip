@@ -27,6 +27,7 @@ struct hpacml_map_s {
     bool fast = false;   // m32 is valid
     bool t32 = false;    // tab is valid: 32-bit view, raw8, at most 64 features
     FeatTable32 tab{};
+    FeatTable32 *tab_dev = nullptr;   // device copy of tab (kernels that index it per thread)
     // snapshot of this (TO) map's inputs for inferences whose outputs may
     // overwrite them: a [points x features] record and a map over it,
     // created on first use
@@ -377,6 +378,7 @@ void hpacml_map_destroy(hpacml_map *m) {
     (void)hipFree(m->feat_dev);
     (void)hipFree(m->base_dev);
     (void)hipFree(m->stride_dev);
+    (void)hipFree(m->tab_dev);
     hpacml_map_destroy(m->snap_map);
     (void)hipFree(m->snap);
     delete m;
@@ -415,8 +417,14 @@ hpacml_status hpacml_map_create(const hpacml_functor *f, int32_t dir, const hpac
         m->dev = make_devmap(m->plan, m->feat_dev, m->base_dev, m->stride_dev);
         m->fast = make_map32(m->plan, &m->m32);
         m->t32 = table32_supported(m->plan, m->fast);
-        if (m->t32)
+        if (m->t32) {
             table32_make(m->plan, &m->tab);
+            s = upload(&m->tab_dev, &m->tab, 1);
+            if (s != HPACML_OK) {
+                hpacml_map_destroy(m);
+                return s;
+            }
+        }
         *out = m;
         return HPACML_OK;
     } catch (const std::bad_alloc &) {
@@ -682,8 +690,8 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
     const CnnPlan &c = model->cnnp;
     const int64_t S = in->plan.n_points / ((int64_t)c.height * c.width);
     if (cnn_use_fused(model, in, out))
-        return hip_status(launch_cnn_fused(in->m32, out->m32, in->tab, out->tab, model->fused, (int32_t)S, c.height,
-                                           c.width, st));
+        return hip_status(launch_cnn_fused(in->m32, out->m32, in->tab_dev, out->tab_dev, model->fused, (int32_t)S,
+                                           c.height, c.width, st));
     // layer by layer: gather every input into the workspace first, so the
     // outputs may overwrite inputs
     hpacml_model *mm = const_cast<hpacml_model *>(model);

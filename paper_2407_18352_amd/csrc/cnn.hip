@@ -9,8 +9,9 @@
 // image.  It gathers the tile plus the stack's total halo through the `to`
 // map into LDS ([row][column][channel], channels padded to 4), then runs every
 // layer over the shrinking region — each layer's output region is the next
-// layer's input region — and the last layer's outputs go straight from
-// registers through the `from` map.  One thread computes one pixel's output
+// layer's input region — and finally writes the last layer's tile through the
+// `from` map (a phase of its own, so the layer loops carry none of the output
+// map's state in registers).  One thread computes one pixel's output
 // channels per pass: 16-byte LDS reads of its window, weights as wave-uniform
 // scalar loads (one FMA per weight per lane), no bank conflicts for 4-channel
 // rows.  Outside the image, a layer's input follows its padding mode:
@@ -29,20 +30,34 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTX = 64;   // tile columns
+constexpr int kPix = 1;   // pixels per thread per pass
 
 // ------------------------------------------------------------------ fused
 struct FusedArgs {
     Map32 in, out;
-    FeatTable32 tin, tout;
+    const FeatTable32 *tin, *tout;   // device; the used entries are staged in LDS
     int32_t S, H, W, n_layers;
     int32_t ty, tiles_x, tiles_y, n_tiles;
     int32_t c0, cout_last, circular, buf1;   // buf1: float offset of the second LDS buffer
+    int32_t co_last_pad;                     // the last layer's channels, padded to 4
     // region of layer l's input (l = n_layers: the tile itself), relative to
     // the tile origin: rows [-rt, ty + rb), columns [-rl, 64 + rr)
     int32_t rt[kCnnFusedMaxLayers + 1], rl[kCnnFusedMaxLayers + 1];
     int32_t rh[kCnnFusedMaxLayers + 1], rw[kCnnFusedMaxLayers + 1];
+    uint32_t rw_magic[kCnnFusedMaxLayers + 1];   // i / rw == (i * rw_magic) >> 24 for i < 2^16
     CnnFusedLayer L[kCnnFusedMaxLayers];
 };
+
+// Feature tables of the two maps in LDS (the first 16 entries): read with a
+// wave-uniform index, so every lane gets the same pointer, without holding
+// 16 pointers per map in scalar registers for the whole kernel.
+struct TabLds {
+    const float *in[kCnnFusedMaxC];
+    float *out[kCnnFusedMaxC];
+    uint32_t in_raw8[kCnnFusedMaxC], out_raw8[kCnnFusedMaxC];
+};
+
+__device__ __forceinline__ int div_region(int i, uint32_t magic) { return (int)(((uint32_t)i * magic) >> 24); }
 
 __device__ __forceinline__ int wrap(int v, int n) {
     int r = v % n;
@@ -52,12 +67,13 @@ __device__ __forceinline__ int wrap(int v, int n) {
 // Layer 0's input region from the `to` map: pixel (y, x) of image s is
 // composed point (s * H + y) * W + x; channel f is its feature f.
 template <int CI>
-__device__ __forceinline__ void gather_region(const FusedArgs &a, int s, int y0, int x0, float *dst) {
+__device__ __forceinline__ void gather_region(const FusedArgs &a, const TabLds &tab, int s, int y0, int x0,
+                                              float *dst) {
     const int rh = a.rh[0], rw = a.rw[0], n = rh * rw;
     const int mode = a.L[0].mode;
     const int vy0 = y0 - a.rt[0], vx0 = x0 - a.rl[0];
     for (int i = threadIdx.x; i < n; i += kThreads) {
-        const int ry = i / rw, rx = i - ry * rw;
+        const int ry = div_region(i, a.rw_magic[0]), rx = i - ry * rw;
         int y = vy0 + ry, x = vx0 + rx;
         bool zero = false;
         if (y < 0 || y >= a.H || x < 0 || x >= a.W) {
@@ -77,8 +93,8 @@ __device__ __forceinline__ void gather_region(const FusedArgs &a, int s, int y0,
         for (int f = 0; f < CI; ++f) {
             v[f] = 0.f;
             if (f < a.c0) {
-                const int fix = edge ? edge_fix32(a.in, pt, a.tin.raw8[f], edge) : 0;
-                v[f] = ldg(a.tin.fptr[f] + (pt.pe + fix));
+                const int fix = edge ? edge_fix32(a.in, pt, tab.in_raw8[f], edge) : 0;
+                v[f] = ldg(tab.in[f] + (pt.pe + fix));
             }
         }
         float4 *d4 = reinterpret_cast<float4 *>(dst + (size_t)i * CI);
@@ -95,6 +111,7 @@ __device__ __forceinline__ void gather_region(const FusedArgs &a, int s, int y0,
 struct LayerRun {
     CnnFusedLayer Ly;
     int oh, ow, sw;        // output region; input region row length
+    uint32_t ow_magic;
     int rt, rl;            // output region origin relative to the tile
     int next_mode, last;
 };
@@ -106,6 +123,7 @@ __device__ __forceinline__ LayerRun layer_run(const FusedArgs &a) {
     r.oh = a.rh[l + 1];
     r.ow = a.rw[l + 1];
     r.sw = a.rw[l];
+    r.ow_magic = a.rw_magic[l + 1];
     r.rt = a.rt[l + 1];
     r.rl = a.rl[l + 1];
     r.last = l == a.n_layers - 1;
@@ -114,13 +132,17 @@ __device__ __forceinline__ LayerRun layer_run(const FusedArgs &a) {
     return r;
 }
 
-// One layer over its output region (the next layer's input region, or the tile).
+// One layer over its output region (the next layer's input region, or the
+// tile for the last layer) into LDS.  Each thread takes kPix pixels per pass
+// (i, i + kThreads, ...): a weight loaded once feeds kPix FMAs.  Pixels
+// outside the image get what the next layer's padding reads there (the last
+// layer's are never stored).
 template <int CIN4, int COUT4>
-__device__ __forceinline__ void conv_pass(const FusedArgs &a, const LayerRun &r, const float *__restrict__ wts,
-                                          const float *src, float *dst, int s, int y0, int x0) {
+__device__ __forceinline__ void conv_pass(const FusedArgs &a, const TabLds &tab, const LayerRun &r,
+                                          const float *__restrict__ wts, const float *src, float *dst, int s, int y0,
+                                          int x0) {
     constexpr int CI = 4 * CIN4, CO = 4 * COUT4;
     const CnnFusedLayer &Ly = r.Ly;
-    const bool last = r.last;
     const int oh = r.oh, ow = r.ow, sw = r.sw;
     const int vy0 = y0 - r.rt, vx0 = x0 - r.rl;
     const int next_mode = r.next_mode;
@@ -128,78 +150,113 @@ __device__ __forceinline__ void conv_pass(const FusedArgs &a, const LayerRun &r,
     const float *bl = wts + Ly.boff;
     const int kh = Ly.kh, kw = Ly.kw;
     const int n = oh * ow;
-    for (int i = threadIdx.x; i < n; i += kThreads) {
-        int ry = i / ow, rx = i - ry * ow;
-        const int vy = vy0 + ry, vx = vx0 + rx;
-        const bool outside = vy < 0 || vy >= a.H || vx < 0 || vx >= a.W;
-        bool zero = false;
-        if (outside && !last && !a.circular) {
-            if (next_mode == HPACML_PADMODE_REPLICATE) {
-                ry = min(max(vy, 0), a.H - 1) - vy0;
-                rx = min(max(vx, 0), a.W - 1) - vx0;
-            } else {
-                zero = true;
-            }
-        }
-        float acc[CO];
+    for (int base = 0; base < n; base += kThreads * kPix) {
+        int off[kPix];          // LDS float offset of each pixel's window origin
+        bool valid[kPix], zero[kPix];
 #pragma unroll
-        for (int co = 0; co < CO; ++co)
-            acc[co] = bl[co];
-        for (int ky = 0; ky < kh; ++ky) {
-            const float *srow = src + (size_t)((ry + ky) * sw + rx) * CI;
-            const float *wrow = wl + ky * kw * CI * CO;
-            for (int kx = 0; kx < kw; ++kx) {
-                const float4 *sp = reinterpret_cast<const float4 *>(srow + kx * CI);
-                const float *wk = wrow + kx * CI * CO;
-                float4 v[CIN4];
-#pragma unroll
-                for (int c4 = 0; c4 < CIN4; ++c4)
-                    v[c4] = sp[c4];
-#pragma unroll
-                for (int c4 = 0; c4 < CIN4; ++c4) {
-                    const float vv[4] = {v[c4].x, v[c4].y, v[c4].z, v[c4].w};
-#pragma unroll
-                    for (int ci = 0; ci < 4; ++ci)
-#pragma unroll
-                        for (int co = 0; co < CO; ++co)
-                            acc[co] = fmaf(wk[(4 * c4 + ci) * CO + co], vv[ci], acc[co]);
+        for (int j = 0; j < kPix; ++j) {
+            const int i = base + j * kThreads + (int)threadIdx.x;
+            valid[j] = i < n;
+            const int ic = valid[j] ? i : n - 1;
+            int ry = div_region(ic, r.ow_magic), rx = ic - ry * ow;
+            const int vy = vy0 + ry, vx = vx0 + rx;
+            const bool outside = vy < 0 || vy >= a.H || vx < 0 || vx >= a.W;
+            zero[j] = false;
+            if (outside && !a.circular) {
+                if (next_mode == HPACML_PADMODE_REPLICATE) {
+                    ry = min(max(vy, 0), a.H - 1) - vy0;
+                    rx = min(max(vx, 0), a.W - 1) - vx0;
+                } else {
+                    zero[j] = true;
                 }
             }
+            off[j] = (ry * sw + rx) * CI;
         }
-        if (Ly.act == HPACML_ACT_RELU) {
+        float acc[kPix][CO];
 #pragma unroll
-            for (int co = 0; co < CO; ++co)
-                acc[co] = relu_arith(acc[co]);
+        for (int co = 0; co < CO; ++co) {
+            const float bv = bl[co];
+#pragma unroll
+            for (int j = 0; j < kPix; ++j)
+                acc[j][co] = bv;
         }
-        if (last) {
-            if (!outside) {
-                const Pt32 pt = locate32(a.out, (s * a.H + vy) * a.W + vx);
-                const uint32_t edge = edge_dims32(a.out, pt);
+        // steps q = (kx, channel group) along a window row: the window values
+        // sit at 4q floats past the row's start and the packed weights
+        // ([ky][kx][ci][co]) at 4q * CO, so one step holds at most 64 weights
+        // in scalar registers whatever the channel counts
+        const int nq = kw * CIN4;
+        for (int ky = 0; ky < kh; ++ky) {
+            const float *wrow = wl + ky * nq * 4 * CO;
+            const int rowoff = ky * sw * CI;
+            for (int q = 0; q < nq; ++q) {
+                const float *wk = wrow + q * 4 * CO;
+                float4 v[kPix];
 #pragma unroll
-                for (int g = 0; g < CO; ++g)
-                    if (g < a.cout_last) {
-                        const int fix = edge ? edge_fix32(a.out, pt, a.tout.raw8[g], edge) : 0;
-                        stg(const_cast<float *>(a.tout.fptr[g]) + (pt.pe + fix), acc[g]);
+                for (int j = 0; j < kPix; ++j)
+                    v[j] = *reinterpret_cast<const float4 *>(src + off[j] + rowoff + 4 * q);
+#pragma unroll
+                for (int ci = 0; ci < 4; ++ci)
+#pragma unroll
+                    for (int co = 0; co < CO; ++co) {
+                        const float wv = wk[ci * CO + co];
+#pragma unroll
+                        for (int j = 0; j < kPix; ++j) {
+                            const float x = ci == 0 ? v[j].x : ci == 1 ? v[j].y : ci == 2 ? v[j].z : v[j].w;
+                            acc[j][co] = fmaf(wv, x, acc[j][co]);
+                        }
                     }
             }
-        } else {
+        }
+#pragma unroll
+        for (int j = 0; j < kPix; ++j) {
+            if (Ly.act == HPACML_ACT_RELU) {
+#pragma unroll
+                for (int co = 0; co < CO; ++co)
+                    acc[j][co] = relu_arith(acc[j][co]);
+            }
+            if (!valid[j])
+                continue;
+            const int i = base + j * kThreads + (int)threadIdx.x;
             float4 *d4 = reinterpret_cast<float4 *>(dst + (size_t)i * CO);
 #pragma unroll
             for (int c4 = 0; c4 < COUT4; ++c4)
-                d4[c4] = zero ? make_float4(0.f, 0.f, 0.f, 0.f)
-                              : make_float4(acc[4 * c4], acc[4 * c4 + 1], acc[4 * c4 + 2], acc[4 * c4 + 3]);
+                d4[c4] = zero[j] ? make_float4(0.f, 0.f, 0.f, 0.f)
+                                 : make_float4(acc[j][4 * c4], acc[j][4 * c4 + 1], acc[j][4 * c4 + 2],
+                                               acc[j][4 * c4 + 3]);
+        }
+    }
+}
+
+// The last layer's tile (LDS, [pixel][4 * cout4]) through the `from` map:
+// pixel (y, x) of image s is point (s * H + y) * W + x, channel g its feature g.
+__device__ __forceinline__ void scatter_tile(const FusedArgs &a, const TabLds &tab, const float *src, int s, int y0,
+                                             int x0) {
+    const int CO = a.co_last_pad;
+    const int n = a.ty * kTX;
+    for (int i = threadIdx.x; i < n; i += kThreads) {
+        const int ry = i / kTX, rx = i % kTX;
+        const int y = y0 + ry, x = x0 + rx;
+        if (y >= a.H || x >= a.W)
+            continue;
+        const Pt32 pt = locate32(a.out, (s * a.H + y) * a.W + x);
+        const uint32_t edge = edge_dims32(a.out, pt);
+        const float *v = src + (size_t)i * CO;
+        for (int g = 0; g < a.cout_last; ++g) {
+            const int fix = edge ? edge_fix32(a.out, pt, tab.out_raw8[g], edge) : 0;
+            stg(tab.out[g] + (pt.pe + fix), v[g]);
         }
     }
 }
 
 template <int CIN4>
-__device__ __forceinline__ void conv_dispatch_out(const FusedArgs &a, const LayerRun &r, const float *__restrict__ wts,
-                                                  const float *src, float *dst, int s, int y0, int x0) {
+__device__ __forceinline__ void conv_dispatch_out(const FusedArgs &a, const TabLds &tab, const LayerRun &r,
+                                                  const float *__restrict__ wts, const float *src, float *dst, int s,
+                                                  int y0, int x0) {
     switch (r.Ly.cout4) {
-    case 1: conv_pass<CIN4, 1>(a, r, wts, src, dst, s, y0, x0); break;
-    case 2: conv_pass<CIN4, 2>(a, r, wts, src, dst, s, y0, x0); break;
-    case 3: conv_pass<CIN4, 3>(a, r, wts, src, dst, s, y0, x0); break;
-    default: conv_pass<CIN4, 4>(a, r, wts, src, dst, s, y0, x0); break;
+    case 1: conv_pass<CIN4, 1>(a, tab, r, wts, src, dst, s, y0, x0); break;
+    case 2: conv_pass<CIN4, 2>(a, tab, r, wts, src, dst, s, y0, x0); break;
+    case 3: conv_pass<CIN4, 3>(a, tab, r, wts, src, dst, s, y0, x0); break;
+    default: conv_pass<CIN4, 4>(a, tab, r, wts, src, dst, s, y0, x0); break;
     }
 }
 
@@ -207,6 +264,15 @@ __global__ void __launch_bounds__(kThreads) cnn_fused_kernel(FusedArgs a, const 
     extern __shared__ float4 lds4[];
     float *const buf0 = reinterpret_cast<float *>(lds4);
     float *const buf1 = buf0 + a.buf1;
+    __shared__ TabLds tab;
+    if (threadIdx.x < kCnnFusedMaxC) {
+        const int f = threadIdx.x;
+        tab.in[f] = a.tin->fptr[f];
+        tab.in_raw8[f] = a.tin->raw8[f];
+        tab.out[f] = const_cast<float *>(a.tout->fptr[f]);
+        tab.out_raw8[f] = a.tout->raw8[f];
+    }
+    __syncthreads();
 
     // blocks of one XCD (blockIdx % 8) take a contiguous range of tiles, so
     // neighbouring tiles share their halo rows in that XCD's L2
@@ -220,10 +286,10 @@ __global__ void __launch_bounds__(kThreads) cnn_fused_kernel(FusedArgs a, const 
     const int y0 = ty_i * a.ty, x0 = (rem - ty_i * a.tiles_x) * kTX;
 
     switch (a.L[0].cin4) {
-    case 1: gather_region<4>(a, s, y0, x0, buf0); break;
-    case 2: gather_region<8>(a, s, y0, x0, buf0); break;
-    case 3: gather_region<12>(a, s, y0, x0, buf0); break;
-    default: gather_region<16>(a, s, y0, x0, buf0); break;
+    case 1: gather_region<4>(a, tab, s, y0, x0, buf0); break;
+    case 2: gather_region<8>(a, tab, s, y0, x0, buf0); break;
+    case 3: gather_region<12>(a, tab, s, y0, x0, buf0); break;
+    default: gather_region<16>(a, tab, s, y0, x0, buf0); break;
     }
     __syncthreads();
     for (int l = 0; l < a.n_layers; ++l) {
@@ -237,13 +303,14 @@ __global__ void __launch_bounds__(kThreads) cnn_fused_kernel(FusedArgs a, const 
         const float *src = (l & 1) ? buf1 : buf0;
         float *dst = (l & 1) ? buf0 : buf1;
         switch (r.Ly.cin4) {
-        case 1: conv_dispatch_out<1>(a, r, wts, src, dst, s, y0, x0); break;
-        case 2: conv_dispatch_out<2>(a, r, wts, src, dst, s, y0, x0); break;
-        case 3: conv_dispatch_out<3>(a, r, wts, src, dst, s, y0, x0); break;
-        default: conv_dispatch_out<4>(a, r, wts, src, dst, s, y0, x0); break;
+        case 1: conv_dispatch_out<1>(a, tab, r, wts, src, dst, s, y0, x0); break;
+        case 2: conv_dispatch_out<2>(a, tab, r, wts, src, dst, s, y0, x0); break;
+        case 3: conv_dispatch_out<3>(a, tab, r, wts, src, dst, s, y0, x0); break;
+        default: conv_dispatch_out<4>(a, tab, r, wts, src, dst, s, y0, x0); break;
         }
         __syncthreads();
     }
+    scatter_tile(a, tab, (a.n_layers & 1) ? buf1 : buf0, s, y0, x0);
 }
 
 // LDS floats of the two buffers for tiles of `ty` rows.
@@ -254,6 +321,8 @@ void fused_regions(const CnnFused &f, int ty, FusedArgs *a, size_t *floats0, siz
     a->rh[L] = ty;
     a->rw[L] = kTX;
     size_t b0 = 0, b1 = 0;
+    // the last layer's output tile
+    ((L & 1) ? b1 : b0) = (size_t)ty * kTX * 4 * f.L[L - 1].cout4;
     for (int l = L - 1; l >= 0; --l) {
         const CnnFusedLayer &y = f.L[l];
         a->rt[l] = a->rt[l + 1] + y.top;
@@ -272,24 +341,35 @@ void fused_regions(const CnnFused &f, int ty, FusedArgs *a, size_t *floats0, siz
     *floats1 = b1;
 }
 
-constexpr size_t kLdsTwoBlocks = 64 * 1024;
+// tile buffers of at most 40 KB leave room for four blocks (16 waves) per CU:
+// measured faster than 64 KB tiles with two blocks, the recomputed halo
+// notwithstanding
+constexpr size_t kLdsShared = 40 * 1024;
 constexpr size_t kLdsOneBlock = 160 * 1024;
 
 // ------------------------------------------------------------------ layers
+// One thread per output pixel and group of up to kConvG output channels
+// (the group is blockIdx.y, so the weights are wave-uniform scalar loads and
+// every input value read feeds kConvG FMAs).
+constexpr int kConvG = 8;
 __global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, const float *__restrict__ in,
-                                                      float *__restrict__ out, int64_t total) {
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= total)
+                                                      float *__restrict__ out, int64_t n_pix) {
+    const int64_t pix = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (pix >= n_pix)
         return;
-    const int co = (int)(idx % L.cout);
-    const int64_t pix = idx / L.cout;
+    const int co0 = blockIdx.y * kConvG;
+    const int ng = min(kConvG, L.cout - co0);
     const int ox = (int)(pix % L.w2);
     const int oy = (int)(pix / L.w2 % L.h2);
     const int64_t s = pix / ((int64_t)L.w2 * L.h2);
     const float *img = in + s * L.h * L.w * L.cin;
     const int y0 = oy * L.sh - (L.same ? (L.kh - 1) / 2 : 0);
     const int x0 = ox * L.sw - (L.same ? (L.kw - 1) / 2 : 0);
-    float acc = L.b[co];
+    const int64_t wstride = (int64_t)L.cin * L.kh * L.kw;   // one output channel's weights
+    float acc[kConvG];
+#pragma unroll
+    for (int g = 0; g < kConvG; ++g)
+        acc[g] = g < ng ? L.b[co0 + g] : 0.f;
     for (int ky = 0; ky < L.kh; ++ky) {
         int y = y0 + ky;
         bool zy = false;
@@ -315,12 +395,19 @@ __global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, const floa
             if (z)
                 continue;
             const float *px = img + ((int64_t)y * L.w + x) * L.cin;
-            const float *wk = L.W + ((int64_t)co * L.cin * L.kh + ky) * L.kw + kx;
-            for (int ci = 0; ci < L.cin; ++ci)
-                acc = fmaf(wk[(int64_t)ci * L.kh * L.kw], px[ci], acc);
+            const float *wk = L.W + (int64_t)co0 * wstride + ky * L.kw + kx;
+            for (int ci = 0; ci < L.cin; ++ci) {
+                const float v = px[ci];
+#pragma unroll
+                for (int g = 0; g < kConvG; ++g)
+                    if (g < ng)
+                        acc[g] = fmaf(wk[g * wstride + (int64_t)ci * L.kh * L.kw], v, acc[g]);
+            }
         }
     }
-    out[idx] = L.act == HPACML_ACT_RELU ? (acc > 0.f ? acc : 0.f) : acc;
+    float *o = out + pix * L.cout + co0;
+    for (int g = 0; g < ng; ++g)
+        o[g] = L.act == HPACML_ACT_RELU ? (acc[g] > 0.f ? acc[g] : 0.f) : acc[g];
 }
 
 __global__ void __launch_bounds__(256) cnn_pool_kernel(CnnLayerDev L, const float *__restrict__ in,
@@ -345,20 +432,68 @@ __global__ void __launch_bounds__(256) cnn_pool_kernel(CnnLayerDev L, const floa
     out[idx] = L.act == HPACML_ACT_RELU ? (m > 0.f ? m : 0.f) : m;
 }
 
+// Fully connected layer over S images: out[S][O] = in[S][K] W^T + b.  A block
+// owns a T x T output tile (T = 64: 4 x 4 outputs per thread; T = 16 for
+// small layers, one output per thread, so that the grid still covers the
+// chip), K in chunks staged in LDS k-major, coalesced loads along k.
+template <int T>
 __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const float *__restrict__ in,
-                                                        float *__restrict__ out, int64_t total) {
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= total)
-        return;
-    const int o = (int)(idx % L.cout);
-    const int64_t s = idx / L.cout;
-    const int64_t n_in = (int64_t)L.h * L.w * L.cin;
-    const float *x = in + s * n_in;
-    const float *w = L.W + o * n_in;
-    float acc = L.b[o];
-    for (int64_t k = 0; k < n_in; ++k)
-        acc = fmaf(w[k], x[k], acc);
-    out[idx] = L.act == HPACML_ACT_RELU ? (acc > 0.f ? acc : 0.f) : acc;
+                                                        float *__restrict__ out, int64_t S) {
+    constexpr int R = T / 16;                 // outputs per thread per dimension
+    constexpr int KC = 256 * 4 / T;           // k per chunk: each thread loads 4 values per operand
+    __shared__ float xs[KC][T + 4];
+    __shared__ float ws[KC][T + 4];
+    const int t = threadIdx.x;
+    const int64_t s0 = (int64_t)blockIdx.x * T;
+    const int o0 = blockIdx.y * T;
+    const int O = L.cout;
+    const int64_t K = (int64_t)L.h * L.w * L.cin;
+    const int ti = t / 16, tj = t % 16;
+    float acc[R][R] = {};
+    for (int64_t k0 = 0; k0 < K; k0 += KC) {
+        // T rows x KC columns of each operand: thread t loads column t % KC of
+        // rows t / KC + (256 / KC) m
+        const int c = t % KC;
+        const int64_t k = k0 + c;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int r = t / KC + (256 / KC) * m;
+            const int64_t sr = s0 + r;
+            const int o = o0 + r;
+            xs[c][r] = (sr < S && k < K) ? in[sr * K + k] : 0.f;
+            ws[c][r] = (o < O && k < K) ? L.W[(int64_t)o * K + k] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll 8
+        for (int kk = 0; kk < KC; ++kk) {
+            float a[R], b[R];
+#pragma unroll
+            for (int i = 0; i < R; ++i) {
+                a[i] = xs[kk][R * ti + i];
+                b[i] = ws[kk][R * tj + i];
+            }
+#pragma unroll
+            for (int i = 0; i < R; ++i)
+#pragma unroll
+                for (int j = 0; j < R; ++j)
+                    acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int64_t sr = s0 + R * ti + i;
+        if (sr >= S)
+            continue;
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+            const int o = o0 + R * tj + j;
+            if (o < O) {
+                const float v = acc[i][j] + L.b[o];
+                out[sr * O + o] = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
+            }
+        }
+    }
 }
 
 __global__ void __launch_bounds__(256) scatter_record_kernel(DevMap m, const float *__restrict__ src) {
@@ -430,7 +565,7 @@ void cnn_fused_pack(const CnnPlan &p, const float *const *W, const float *const 
 
 int cnn_fused_tile_rows(const CnnFused &f, int32_t H) {
     // the largest tile of at most max(H, 1) rows (rounded up to a power of
-    // two) whose buffers leave room for two blocks per CU, else for one
+    // two) whose buffers fit kLdsShared, else one block per CU
     int one = 0;
     for (int ty : {32, 16, 8, 4, 2, 1}) {
         if (ty > 1 && ty / 2 >= H)
@@ -439,7 +574,7 @@ int cnn_fused_tile_rows(const CnnFused &f, int32_t H) {
         size_t f0, f1;
         fused_regions(f, ty, &a, &f0, &f1);
         const size_t bytes = (f0 + f1) * sizeof(float);
-        if (bytes <= kLdsTwoBlocks)
+        if (bytes <= kLdsShared)
             return ty;
         if (!one && bytes <= kLdsOneBlock)
             one = ty;
@@ -447,7 +582,7 @@ int cnn_fused_tile_rows(const CnnFused &f, int32_t H) {
     return one;
 }
 
-hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32 *tin, const FeatTable32 *tout,
                             const CnnFused &f, int32_t S, int32_t H, int32_t W, hipStream_t stream) {
     const int ty = cnn_fused_tile_rows(f, H);
     if (ty == 0)
@@ -472,12 +607,20 @@ hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32
     a.n_tiles = (int32_t)n_tiles;
     a.c0 = f.c0;
     a.cout_last = f.cout_last;
+    a.co_last_pad = 4 * f.L[f.n_layers - 1].cout4;
     a.circular = f.circular;
     for (int l = 0; l < f.n_layers; ++l)
         a.L[l] = f.L[l];
     size_t f0, f1;
     fused_regions(f, ty, &a, &f0, &f1);
     a.buf1 = (int32_t)f0;
+    for (int l = 0; l <= f.n_layers; ++l) {
+        // region sizes stay below 2^16 pixels and widths at most 256 (checked
+        // here): the multiply-shift quotient is then exact
+        if ((int64_t)a.rh[l] * a.rw[l] >= (1 << 16) || a.rw[l] > 256)
+            return hipErrorInvalidValue;
+        a.rw_magic[l] = (uint32_t)(((1u << 24) + a.rw[l] - 1) / a.rw[l]);
+    }
     const size_t lds = (f0 + f1) * sizeof(float);
     hipError_t e = hipFuncSetAttribute((const void *)cnn_fused_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)lds);
@@ -495,15 +638,33 @@ hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, i
     if (blocks > INT32_MAX)
         return hipErrorInvalidValue;
     switch (L.kind) {
-    case HPACML_LAYER_CONV2D:
-        hipLaunchKernelGGL(cnn_conv_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, L, in, out, total);
+    case HPACML_LAYER_CONV2D: {
+        const int64_t n_pix = S * (int64_t)L.h2 * L.w2;
+        const int64_t bx = (n_pix + 255) / 256, by = (L.cout + kConvG - 1) / kConvG;
+        if (bx > INT32_MAX || by > 65535)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL(cnn_conv_kernel, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, in, out,
+                           n_pix);
         break;
+    }
     case HPACML_LAYER_MAXPOOL2D:
         hipLaunchKernelGGL(cnn_pool_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, L, in, out, total);
         break;
-    default:
-        hipLaunchKernelGGL(cnn_linear_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, L, in, out, total);
+    default: {
+        // 64 x 64 tiles when they still give two blocks per CU, else 16 x 16
+        const bool big = ((S + 63) / 64) * ((L.cout + 63) / 64) >= 512;
+        const int T = big ? 64 : 16;
+        const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
+        if (bx > INT32_MAX || by > 65535)
+            return hipErrorInvalidValue;
+        if (big)
+            hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, in,
+                               out, S);
+        else
+            hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, in,
+                               out, S);
         break;
+    }
     }
     return hipGetLastError();
 }

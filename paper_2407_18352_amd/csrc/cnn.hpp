@@ -42,7 +42,8 @@ void cnn_fused_pack(const CnnPlan &p, const float *const *W, const float *const 
                     CnnFused *out);
 // Rows per tile (64 columns) for this stack, or 0 when no tile fits in LDS.
 int cnn_fused_tile_rows(const CnnFused &f, int32_t H);
-hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+// tin, tout: device copies of the maps' feature tables
+hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32 *tin, const FeatTable32 *tout,
                             const CnnFused &f, int32_t S, int32_t H, int32_t W, hipStream_t stream);
 
 }  // namespace hpacml

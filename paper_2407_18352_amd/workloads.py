@@ -326,6 +326,23 @@ def video_frames(cfg: int, k: int, S: int, H: int, W: int) -> np.ndarray:
     return f
 
 
+def cnn_model(name: str, size=None) -> dict:
+    """The model of a convolutional workload alone (no input arrays)."""
+    cfg = 10 + CNN_NAMES.index(name)
+    size = CNN_FULL[name] if size in (None, "full") else CNN_SMALL[name] if size == "small" else size
+    if name == "weather_cnn":
+        ny, nx = size
+        layers = [conv_layer(cfg, 100, 4, 8, (5, 5)), conv_layer(cfg, 110, 8, 4, (3, 3), act=IDENTITY)]
+        return {"kind": "cnn", "in_channels": 4, "image": (ny, nx), "layers": layers, "compute": "f32"}
+    S, H, W = size
+    c1 = conv_layer(cfg, 100, 1, 8, (4, 4), padding="valid", mode="zeros", stride=(4, 4))
+    h, w = (H - 4) // 4 + 1, (W - 4) // 4 + 1
+    h, w = (h - 2) // 2 + 1, (w - 2) // 2 + 1
+    layers = [c1, {"kind": "pool", "kernel": (2, 2), "act": IDENTITY},
+              linear_layer(cfg, 110, h * w * 8, 64), linear_layer(cfg, 120, 64, 2, act=IDENTITY)]
+    return {"kind": "cnn", "in_channels": 1, "image": (H, W), "layers": layers, "compute": "f32"}
+
+
 def make_cnn(name: str, size=None) -> Workload:
     """A convolutional workload; ``model`` is ``{"kind": "cnn", "in_channels",
     "image": (rows, columns), "layers": [...]}`` (the layer dicts of
@@ -335,23 +352,16 @@ def make_cnn(name: str, size=None) -> Workload:
         size = CNN_FULL[name]
     elif size == "small":
         size = CNN_SMALL[name]
+    model = cnn_model(name, size)
     if name == "weather_cnn":
         ny, nx = size
         inputs = [sinusoid_field(cfg, k, ny, nx) for k in range(4)]
-        layers = [conv_layer(cfg, 100, 4, 8, (5, 5)), conv_layer(cfg, 110, 8, 4, (3, 3), act=IDENTITY)]
-        model = {"kind": "cnn", "in_channels": 4, "image": (ny, nx), "layers": layers, "compute": "f32"}
         ins, outs = point2d_spec(ny, nx), point2d_spec(ny, nx)
         outputs = [sentinel_like((ny, nx)) for _ in range(4)]
         dims = [4, 4]
     elif name == "particle_cnn":
         S, H, W = size
         inputs = [video_frames(cfg, 0, S, H, W)]
-        c1 = conv_layer(cfg, 100, 1, 8, (4, 4), padding="valid", mode="zeros", stride=(4, 4))
-        h, w = (H - 4) // 4 + 1, (W - 4) // 4 + 1
-        h, w = (h - 2) // 2 + 1, (w - 2) // 2 + 1
-        layers = [c1, {"kind": "pool", "kernel": (2, 2), "act": IDENTITY},
-                  linear_layer(cfg, 110, h * w * 8, 64), linear_layer(cfg, 120, 64, 2, act=IDENTITY)]
-        model = {"kind": "cnn", "in_channels": 1, "image": (H, W), "layers": layers, "compute": "f32"}
         ins = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
                "bnd": [NONE] * 3}
         outs = pointwise_spec(S)

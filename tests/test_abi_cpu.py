@@ -200,8 +200,7 @@ def test_cnn_validate_shapes_and_errors():
     """Convolutional model descriptions: output shapes of the two workload
     stacks, and each rejected form reported without a device."""
     for name, want in [("weather_cnn", (2048, 2048, 4)), ("particle_cnn", (1, 1, 2))]:
-        w = wl.make_cnn(name, "full") if name == "particle_cnn" else wl.make_cnn(name, (2048, 2048))
-        st, shp = api.validate_cnn(w.model)
+        st, shp = api.validate_cnn(wl.cnn_model(name, "full"))
         assert st == _abi.OK and shp == want, name
     conv = wl.conv_layer(1, 0, 4, 8, (3, 3))
     base = {"kind": "cnn", "in_channels": 4, "image": (16, 16), "layers": [conv]}

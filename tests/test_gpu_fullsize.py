@@ -63,3 +63,24 @@ def test_collect_stencil3d_slabs_bitexact(z0, z1):
     spec = dict(w.in_spec, sweep=((z0, 0, 0), (z1, 512, 512), (1, 1, 1)))
     got = run_collect(spec, w.inputs)
     assert np.array_equal(got, oracle.collect(spec, w.inputs))
+
+
+@pytest.mark.parametrize("name", wl.CNN_NAMES)
+def test_cnn_fullsize(name):
+    """The convolutional workloads at full size in the benchmark's launch
+    configuration, against the oracle over whole images: every pixel of the
+    2048 x 2048 step (4.2 G multiply-adds in fp64), every frame estimate."""
+    w = wl.make_cnn(name)
+    import torch
+    ins = [torch.from_numpy(a).cuda() for a in w.inputs]
+    outs = [torch.from_numpy(a).cuda() for a in w.outputs]
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.FROM)
+    m = api.CnnModel(w.model)
+    var = api.variant(m, mi, mo)
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    got = np.stack([o.cpu().numpy().reshape(-1) for o in outs], 1)
+    Y = oracle.cnn(w.model, oracle.gather(w.in_spec, w.inputs))
+    worst, norm = assert_close(got, Y, RTOL["f32"], "%s full via %s" % (name, var))
+    print("%s full [%s]: worst scaled %.3e, normwise %.3e" % (name, var, worst, norm))
