@@ -279,6 +279,68 @@ hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *
 hpacml_status hpacml_collect_pair(const hpacml_map *a, float *dst_a, int64_t ld_a,
                                   const hpacml_map *b, float *dst_b, int64_t ld_b, void *stream);
 
+/* ---- execution control and the collection sink ---------------------------
+ * A region ties the `to` map, the `from` map and the model of one annotated
+ * code block together with the `ml` clause's mode (Sec. III-C, Fig. 3:
+ * `ml(infer | collect | predicated[:cond]) ... if(cond)`; Sec. IV-B):
+ *   INFER      every invocation runs hpacml_infer;
+ *   COLLECT    every invocation records the inputs through the `to` map, runs
+ *              the accurate path (the region's original code), records the
+ *              outputs through the `from` map and the accurate path's time;
+ *   PREDICATED per invocation: `cond` nonzero -> INFER, zero -> COLLECT.
+ * The `if` clause (`enabled` = 0) runs the accurate path alone: no inference,
+ * no recording.  Records go to a sink of `capacity` samples in device memory
+ * (one sample per collected invocation: inputs [points(in)][F_in], outputs
+ * [points(out)][F_out], the accurate path's time), the datasets of one region
+ * group in the paper's database (Sec. IV-B). */
+enum { HPACML_MODE_INFER = 0, HPACML_MODE_COLLECT = 1, HPACML_MODE_PREDICATED = 2 };
+
+/* The accurate path: the region's original code, which must enqueue its work
+ * on `stream` (a hipStream_t) and return; called on the calling thread. */
+typedef void (*hpacml_accurate_fn)(void *user, void *stream);
+
+typedef struct hpacml_region_s hpacml_region;
+
+/* Creates a region.  The maps and the model are borrowed (keep them alive
+ * while the region is used); `in` is a TO map, `out` a FROM map, with the
+ * shapes hpacml_infer requires of them and `model` (checked here: the status
+ * hpacml_infer would return, without launching).  capacity >= 0 samples are
+ * allocated up front on the current device (0 for INFER regions);
+ * HPACML_E_NOMEM if they do not fit. */
+hpacml_status hpacml_region_create(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out,
+                                   int32_t mode, int64_t capacity, hpacml_region **region);
+
+/* One invocation of the region on `stream`.  Collecting into a full sink
+ * returns HPACML_E_RANGE before anything is enqueued or called; a collecting
+ * invocation needs `accurate` (HPACML_E_INVAL when NULL), as does enabled == 0.
+ * Asynchronous like hpacml_infer / hpacml_collect; the accurate path's time is
+ * measured with events around the callback's work on `stream`. */
+hpacml_status hpacml_region_run(hpacml_region *region, int32_t cond, int32_t enabled,
+                                hpacml_accurate_fn accurate, void *user, void *stream);
+
+/* Number of samples collected so far. */
+hpacml_status hpacml_region_samples(const hpacml_region *region, int64_t *n_samples);
+
+/* Copies the first n samples to HOST buffers (any may be NULL):
+ * inputs [n][points(in)][F_in], outputs [n][points(out)][F_out], times_ms [n].
+ * Waits for the region's work.  n > samples collected: HPACML_E_RANGE. */
+hpacml_status hpacml_region_read(const hpacml_region *region, int64_t n, float *inputs, float *outputs,
+                                 float *times_ms);
+
+/* Writes the collected samples as one region group of the database: the
+ * directory `dir`/`name`/ with inputs.npy [n][points(in)][F_in], outputs.npy
+ * [n][points(out)][F_out] and time.npy [n] (milliseconds), NumPy's .npy format
+ * (float32, C order), the outer dimension numbering the samples.  Creates the
+ * two directories if needed.  HPACML_E_INVAL for an unwritable path. */
+hpacml_status hpacml_region_save(const hpacml_region *region, const char *dir, const char *name);
+
+/* Forgets the collected samples (the sink is reused from sample 0). */
+hpacml_status hpacml_region_reset(hpacml_region *region);
+
+/* Frees a region and its sink (not its maps or model).  NULL-safe.
+ * Synchronise the streams that use it first. */
+void hpacml_region_destroy(hpacml_region *region);
+
 /* Name of the kernel hpacml_infer would launch for these handles (a static
  * string, prefixed "snapshot+" when the inputs are copied first), or NULL
  * when the arguments are invalid.  Allocates nothing. */

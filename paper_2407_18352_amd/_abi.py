@@ -12,6 +12,7 @@ BND_NONE, BND_PERIODIC, BND_CLAMP = 0, 1, 2
 F32, BF16 = 0, 1
 ACT_IDENTITY, ACT_RELU = 0, 1
 LAYER_CONV2D, LAYER_MAXPOOL2D, LAYER_LINEAR = 0, 1, 2
+MODE_INFER, MODE_COLLECT, MODE_PREDICATED = 0, 1, 2
 PAD_VALID, PAD_SAME = 0, 1
 PADMODE_ZEROS, PADMODE_CIRCULAR, PADMODE_REPLICATE = 0, 1, 2
 
@@ -42,6 +43,9 @@ class Layer(C.Structure):
                 ("stride", C.c_int32 * 2), ("padding", C.c_int32), ("pad_mode", C.c_int32), ("act", C.c_int32)]
 
 
+# hpacml_accurate_fn: void (*)(void *user, void *stream)
+ACCURATE_FN = C.CFUNCTYPE(None, C.c_void_p, C.c_void_p)
+
 # every symbol the header declares, with (restype, argtypes)
 _P = C.POINTER
 SIGNATURES = {
@@ -65,6 +69,14 @@ SIGNATURES = {
     "hpacml_cnn_validate": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(C.c_int32)]),
     "hpacml_cnn_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(_P(C.c_float)),
                                     _P(_P(C.c_float)), C.c_int32, _P(C.c_void_p)]),
+    "hpacml_region_create": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int64,
+                                       _P(C.c_void_p)]),
+    "hpacml_region_run": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, ACCURATE_FN, C.c_void_p, C.c_void_p]),
+    "hpacml_region_samples": (C.c_int, [C.c_void_p, _P(C.c_int64)]),
+    "hpacml_region_read": (C.c_int, [C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p]),
+    "hpacml_region_save": (C.c_int, [C.c_void_p, C.c_char_p, C.c_char_p]),
+    "hpacml_region_reset": (C.c_int, [C.c_void_p]),
+    "hpacml_region_destroy": (None, [C.c_void_p]),
 }
 
 _lib = None

@@ -249,3 +249,71 @@ def collect_pair(a: Map, dst_a, ld_a: int, b: Map, dst_b, ld_b: int, stream=None
 def variant(model: Model, in_map: Map, out_map: Map) -> str:
     r = lib().hpacml_infer_variant(model.handle, in_map.handle, out_map.handle)
     return r.decode() if r else None
+
+
+class Region:
+    """Execution control of one annotated region (``ml(infer | collect |
+    predicated)`` and ``if``): ``run`` infers, or records the inputs, calls
+    ``accurate(stream_handle)`` (the region's original code, which enqueues its
+    work on that stream) and records the outputs and the accurate path's time
+    into a sink of ``capacity`` samples."""
+
+    def __init__(self, model, in_map: Map, out_map: Map, mode: int, capacity: int = 0):
+        h = C.c_void_p()
+        check(lib().hpacml_region_create(model.handle, in_map.handle, out_map.handle, int(mode), int(capacity),
+                                         C.byref(h)), "hpacml_region_create")
+        self.handle = h
+        self.keep = (model, in_map, out_map)
+        self.points, self.f_in = in_map.n_points, in_map.n_features
+        self.points_out, self.f_out = out_map.n_points, out_map.n_features
+
+    def run(self, accurate=None, cond: bool = True, enabled: bool = True, stream=None) -> None:
+        """``accurate(stream_handle)`` gets the stream as an int (0: the null
+        stream); an exception it raises is re-raised here once the library
+        call has returned."""
+        errors = []
+
+        def call(user, st):
+            try:
+                accurate(st or 0)
+            except BaseException as e:   # must not unwind through the C frame
+                errors.append(e)
+        cb = _abi.ACCURATE_FN(call) if accurate is not None else _abi.ACCURATE_FN()
+        check(lib().hpacml_region_run(self.handle, 1 if cond else 0, 1 if enabled else 0, cb, None,
+                                      _stream(stream)), "hpacml_region_run")
+        if errors:
+            raise errors[0]
+
+    @property
+    def samples(self) -> int:
+        n = C.c_int64()
+        check(lib().hpacml_region_samples(self.handle, C.byref(n)), "hpacml_region_samples")
+        return n.value
+
+    def read(self):
+        """(inputs [n, points, F_in], outputs [n, points_out, F_out], times_ms [n]) as numpy."""
+        import numpy as np
+        n = self.samples
+        ins = np.zeros((n, self.points, self.f_in), np.float32)
+        outs = np.zeros((n, self.points_out, self.f_out), np.float32)
+        t = np.zeros(n, np.float32)
+        check(lib().hpacml_region_read(self.handle, n, ins.ctypes.data, outs.ctypes.data, t.ctypes.data),
+              "hpacml_region_read")
+        return ins, outs, t
+
+    def save(self, directory: str, name: str) -> None:
+        check(lib().hpacml_region_save(self.handle, directory.encode(), name.encode()), "hpacml_region_save")
+
+    def reset(self) -> None:
+        check(lib().hpacml_region_reset(self.handle), "hpacml_region_reset")
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().hpacml_region_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

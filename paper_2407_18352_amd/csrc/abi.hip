@@ -175,6 +175,10 @@ hpacml_status check_infer(const hpacml_model *model, const hpacml_map *in, const
 
 }  // namespace
 
+hpacml_status hpacml::infer_status(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+    return check_infer(model, in, out);
+}
+
 namespace hpacml {
 
 DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const *base_dev,

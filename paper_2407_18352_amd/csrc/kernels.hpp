@@ -96,4 +96,7 @@ hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const FeatTable32 
                            const BF16Packed &pk, hipStream_t stream);
 const char *bf16_variant_name(const BF16Packed &pk);
 
+// The status hpacml_infer would return for these handles, without launching.
+hpacml_status infer_status(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out);
+
 }  // namespace hpacml

@@ -1,0 +1,194 @@
+"""GPU tests of region execution control (``ml(infer | collect | predicated)``
+and ``if``) and of the collection sink, through the C ABI.  The accurate path
+is a stand-in that writes a known pattern, so recorded outputs have exact
+expected values; recorded inputs are compared bit for bit with the oracle's
+collect of the same arrays."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2407_18352_amd import _abi, api
+from paper_2407_18352_amd import workloads as wl
+from gpu_util import RTOL, assert_close, require_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+class Setup:
+    """A bond-pricing region of n points: 9 input arrays, 1 output array."""
+
+    def __init__(self, n=5003):
+        self.w = wl.make("bonds", n)
+        self.ins = to_dev(self.w.inputs)
+        self.outs = to_dev(self.w.outputs)
+        self.mi = api.Map(self.w.in_spec, self.ins, _abi.TO)
+        self.mo = api.Map(self.w.out_spec, self.outs, _abi.FROM)
+        self.model = api.Model(self.w.model)
+        self.calls = 0
+
+    def pattern(self, k):
+        return (np.arange(self.w.n_points, dtype=np.float32) * np.float32(0.5) + np.float32(k)).astype(np.float32)
+
+    def accurate(self, k):
+        """The region's original code: out[i] = 0.5 i + k, on the given stream."""
+        import torch
+
+        def run(stream_handle):
+            self.calls += 1
+            st = torch.cuda.ExternalStream(stream_handle) if stream_handle else torch.cuda.default_stream()
+            with torch.cuda.stream(st):
+                self.outs[0].copy_(torch.from_numpy(self.pattern(k)).cuda(non_blocking=False))
+        return run
+
+    def host_inputs(self):
+        return [t.cpu().numpy() for t in self.ins]
+
+
+def test_infer_mode_is_hpacml_infer():
+    import torch
+    s = Setup()
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_INFER)
+    r.run()
+    torch.cuda.synchronize()
+    got = s.outs[0].cpu().numpy().copy()
+    s.outs[0].fill_(0)
+    api.infer(s.model, s.mi, s.mo)
+    torch.cuda.synchronize()
+    assert np.array_equal(got.view(np.uint32), s.outs[0].cpu().numpy().view(np.uint32))
+    assert r.samples == 0
+
+
+def test_collect_mode_records_inputs_outputs_and_time():
+    import torch
+    s = Setup()
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_COLLECT, capacity=3)
+    expect_in = []
+    for k in range(3):
+        # new inputs per invocation (the application's state changes)
+        for t in s.ins:
+            t.mul_(1.25).add_(0.5)
+        torch.cuda.synchronize()
+        expect_in.append(oracle.collect(s.w.in_spec, s.host_inputs()))
+        r.run(s.accurate(k))
+    assert s.calls == 3 and r.samples == 3
+    ins, outs, t = r.read()
+    for k in range(3):
+        assert np.array_equal(ins[k].view(np.uint32), expect_in[k]), k
+        assert np.array_equal(outs[k, :, 0], s.pattern(k)), k
+    assert np.all(t > 0) and np.all(np.isfinite(t))
+
+
+def test_predicated_toggles_inference_and_collection():
+    import torch
+    s = Setup()
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_PREDICATED, capacity=4)
+    Y = oracle.infer_rows(s.w.in_spec, s.w.inputs, s.w.model)
+    for k, cond in enumerate([True, False, True, False]):
+        r.run(s.accurate(k), cond=cond)
+        torch.cuda.synchronize()
+        got = s.outs[0].cpu().numpy()
+        if cond:
+            assert_close(got[:, None], Y, RTOL["f32"], "inference invocation %d" % k)
+        else:
+            assert np.array_equal(got, s.pattern(k))
+    assert s.calls == 2 and r.samples == 2
+    _, outs, _ = r.read()
+    assert np.array_equal(outs[0, :, 0], s.pattern(1)) and np.array_equal(outs[1, :, 0], s.pattern(3))
+
+
+def test_if_false_runs_the_accurate_path_only():
+    import torch
+    s = Setup()
+    for mode in (_abi.MODE_INFER, _abi.MODE_COLLECT, _abi.MODE_PREDICATED):
+        r = api.Region(s.model, s.mi, s.mo, mode, capacity=2)
+        r.run(s.accurate(7), cond=True, enabled=False)
+        torch.cuda.synchronize()
+        assert np.array_equal(s.outs[0].cpu().numpy(), s.pattern(7))
+        assert r.samples == 0
+        r.close()
+
+
+def test_full_sink_is_an_error_before_anything_runs_and_reset_reuses_it():
+    import torch
+    s = Setup(300)
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_COLLECT, capacity=2)
+    r.run(s.accurate(0))
+    r.run(s.accurate(1))
+    with pytest.raises(_abi.HpacmlError) as e:
+        r.run(s.accurate(2))
+    assert e.value.status == _abi.E_RANGE and s.calls == 2
+    r.reset()
+    assert r.samples == 0
+    r.run(s.accurate(5))
+    torch.cuda.synchronize()
+    _, outs, _ = r.read()
+    assert outs.shape == (1, 300, 1) and np.array_equal(outs[0, :, 0], s.pattern(5))
+    # collecting needs the accurate path
+    with pytest.raises(_abi.HpacmlError) as e:
+        r.run(None)
+    assert e.value.status == _abi.E_INVAL
+
+
+def test_save_writes_the_region_group_as_npy(tmp_path):
+    s = Setup(1000)
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_COLLECT, capacity=2)
+    r.run(s.accurate(0))
+    r.run(s.accurate(1))
+    ins, outs, t = r.read()
+    r.save(str(tmp_path / "db"), "bonds_region")
+    g = tmp_path / "db" / "bonds_region"
+    a = np.load(g / "inputs.npy")
+    b = np.load(g / "outputs.npy")
+    c = np.load(g / "time.npy")
+    assert a.dtype == np.float32 and a.shape == (2, 1000, 9) and np.array_equal(a, ins)
+    assert b.shape == (2, 1000, 1) and np.array_equal(b, outs)
+    assert c.shape == (2,) and np.array_equal(c, t)
+    with pytest.raises(_abi.HpacmlError) as e:
+        r.save(str(tmp_path / "db"), "a/b")
+    assert e.value.status == _abi.E_INVAL
+
+
+def test_region_create_errors():
+    s = Setup(500)
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.Region(s.model, s.mi, s.mo, 7)
+    assert e.value.status == _abi.E_INVAL
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.Region(s.model, s.mo, s.mi, _abi.MODE_INFER)      # directions swapped
+    assert e.value.status == _abi.E_INVAL
+    other = api.Model(wl.make_model(2, [9, 32, 2], "f32"))
+    with pytest.raises(_abi.HpacmlError) as e:
+        api.Region(other, s.mi, s.mo, _abi.MODE_COLLECT, capacity=1)
+    assert e.value.status == _abi.E_SHAPE
+
+
+def test_collect_around_a_convolutional_region():
+    """A ParticleFilter-like region: frames in, one 2-value estimate per frame
+    out; the two datasets have different point counts."""
+    import torch
+    w = wl.make_cnn("particle_cnn", (3, 64, 64))
+    ins, outs = to_dev(w.inputs), to_dev(w.outputs)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.FROM)
+    m = api.CnnModel(w.model)
+    r = api.Region(m, mi, mo, _abi.MODE_PREDICATED, capacity=1)
+
+    def accurate(handle):
+        for k, o in enumerate(outs):
+            o.fill_(float(k + 1))
+    r.run(accurate, cond=False)
+    r.run(None, cond=True)
+    torch.cuda.synchronize()
+    ins_rec, outs_rec, _ = r.read()
+    assert ins_rec.shape == (1, 3 * 64 * 64, 1) and outs_rec.shape == (1, 3, 2)
+    assert np.array_equal(ins_rec[0, :, 0], w.inputs[0].reshape(-1))
+    assert np.array_equal(outs_rec[0], np.array([[1, 2]] * 3, np.float32))
+    exp = [o.copy() for o in w.outputs]
+    oracle.infer(w.in_spec, w.inputs, w.out_spec, exp, w.model)
+    got = np.stack([o.cpu().numpy() for o in outs], 1)
+    assert_close(got, np.stack(exp, 1), RTOL["f32"], "convolutional inference through a region")
