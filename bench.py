@@ -86,6 +86,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="bonds", choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--inplace", action="store_true",
+                    help="write the outputs back into the input fields (a time step advanced in place: windowed "
+                         "maps then run the snapshot pass); no oracle leg, the fields change every step")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="before warm-up, run one device-to-device copy of this many MiB (a kernel of "
@@ -114,6 +117,12 @@ def main():
 
     ins = [torch.from_numpy(a).cuda() for a in w.inputs]
     outs = [torch.from_numpy(a).cuda() for a in w.outputs]
+    if args.inplace:
+        if len(w.outputs) > len(ins) or any(o.shape != i.shape for o, i in zip(outs, ins)):
+            print("--inplace needs outputs shaped like the first inputs", file=sys.stderr)
+            sys.exit(2)
+        outs = ins[:len(w.outputs)]
+        args.no_cpu_baseline = True
     mi = api.Map(w.in_spec, ins, _abi.TO)
     mo = api.Map(w.out_spec, outs, _abi.FROM)
     mo_rec = api.Map(w.out_spec, outs, _abi.TO)        # the outputs as a recorded map
@@ -188,8 +197,9 @@ def main():
         "vs_baseline": None,
         "dtype": w.compute,
         "data": "synthetic (seeded generators; random-init He-normal weights)",
-        "config": {"workload": DESCRIPTION[args.workload], "points": B, "features_in": Fi,
-                   "features_out": Fo, "output_points": Bo},
+        "config": {"workload": DESCRIPTION[args.workload] + ("; outputs written in place into the input fields"
+                                                              if args.inplace else ""),
+                   "points": B, "features_in": Fi, "features_out": Fo, "output_points": Bo},
         "roofline": {"bound": bound, "achieved": achieved / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
                      "frac": achieved / peak, "traffic": traffic["bytes"] if traffic else None,
                      "traffic_source": traffic["source"] if traffic else None,

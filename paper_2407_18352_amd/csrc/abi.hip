@@ -737,29 +737,47 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
 
 namespace {
 
-// The snapshot record of a TO map ([points x features], row-major, at `buf`)
-// and the map that reads it back: one rank-2 target [B, F] whose point b
-// reads the row (b, 0..F-1).
+// The snapshot record of a TO map and the map that reads it back.  Feature-
+// major ([F][B]: F targets of B points, so every element index stays below B
+// and the map keeps the 32-bit form however large B * F is) when the `to` map
+// itself has the 32-bit form (its collect can write that layout); otherwise
+// row-major [B][F] read as one rank-2 target whose point b is the row
+// (b, 0..F-1).
+bool snapshot_feature_major(const hpacml_map *in) { return in->t32 && in->plan.n_features > 1; }
+
 struct SnapshotDesc {
     hpacml_slice sl{};
     hpacml_functor fn{};
-    hpacml_array a{};
+    std::vector<hpacml_array> a;
     hpacml_sweep sw{};
     int32_t bnd[HPACML_MAX_RANK] = {HPACML_BND_NONE, HPACML_BND_NONE, HPACML_BND_NONE, HPACML_BND_NONE};
 
-    SnapshotDesc(int64_t B, int32_t F, float *buf) {
-        sl.count[0] = 1;
-        sl.count[1] = F;
-        fn = hpacml_functor{2, 1, &sl, F};
-        a.data = buf;
-        a.dtype = HPACML_F32;
-        a.extent[0] = B;
-        a.extent[1] = F;
-        a.stride[0] = F;
-        a.stride[1] = 1;
-        sw.stop[0] = B;
-        sw.stop[1] = 1;
+    SnapshotDesc(int64_t B, int32_t F, float *buf, bool feature_major) {
         sw.step[0] = sw.step[1] = 1;
+        sw.stop[0] = B;
+        if (feature_major) {
+            sl.count[0] = 1;
+            fn = hpacml_functor{1, 1, &sl, F};
+            a.resize(F);
+            for (int f = 0; f < F; ++f) {
+                a[f].data = buf + (size_t)f * B;
+                a[f].dtype = HPACML_F32;
+                a[f].extent[0] = B;
+                a[f].stride[0] = 1;
+            }
+        } else {
+            sl.count[0] = 1;
+            sl.count[1] = F;
+            fn = hpacml_functor{2, 1, &sl, F};
+            a.resize(1);
+            a[0].data = buf;
+            a[0].dtype = HPACML_F32;
+            a[0].extent[0] = B;
+            a[0].extent[1] = F;
+            a[0].stride[0] = F;
+            a[0].stride[1] = 1;
+            sw.stop[1] = 1;
+        }
     }
 };
 
@@ -776,9 +794,10 @@ hpacml_status snapshot_map(const hpacml_map *in, const hpacml_map **out) {
             (void)hipGetLastError();
             return hip_status(e);
         }
-        const SnapshotDesc d(B, F, buf);
+        const SnapshotDesc d(B, F, buf, snapshot_feature_major(in));
         hpacml_map *m = nullptr;
-        hpacml_status s = hpacml_map_create(&d.fn, HPACML_TO, &d.a, 1, &d.sw, d.bnd, &m);
+        hpacml_status s =
+            hpacml_map_create(&d.fn, HPACML_TO, d.a.data(), (int32_t)d.a.size(), &d.sw, d.bnd, &m);
         if (s != HPACML_OK) {
             (void)hipFree(buf);
             return s;
@@ -798,10 +817,11 @@ bool snapshot_t32(const hpacml_map *in) {
             return in->snap_map->t32;
     }
     // any non-null address serves the host-side plan
-    const SnapshotDesc d(in->plan.n_points, in->plan.n_features, (float *)in->plan.base[0]);
+    const SnapshotDesc d(in->plan.n_points, in->plan.n_features, (float *)in->plan.base[0],
+                         snapshot_feature_major(in));
     MapPlan p;
     Map32 m32;
-    if (build_map_plan(&d.fn, HPACML_TO, &d.a, 1, &d.sw, d.bnd, &p) != HPACML_OK)
+    if (build_map_plan(&d.fn, HPACML_TO, d.a.data(), (int32_t)d.a.size(), &d.sw, d.bnd, &p) != HPACML_OK)
         return false;
     return table32_supported(p, make_map32(p, &m32));
 }
@@ -853,8 +873,16 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
         // then reads them from there (stream order separates the two passes)
         const hpacml_map *sm = nullptr;
         s = snapshot_map(in, &sm);
-        if (s == HPACML_OK)
-            s = hpacml_collect(in, in->snap, in->plan.n_features, stream);
+        if (s == HPACML_OK) {
+            if (snapshot_feature_major(in)) {
+                CollectJob32 j = collect32_job(in->plan, in->m32, in->tab, (uint32_t *)in->snap, 1);
+                j.dense = 0;
+                j.fs = in->plan.n_points;
+                s = hip_status(launch_collect32(&j, 1, st));
+            } else {
+                s = hpacml_collect(in, in->snap, in->plan.n_features, stream);
+            }
+        }
         if (s != HPACML_OK)
             return s;
         in = sm;

@@ -159,7 +159,12 @@ __device__ __forceinline__ void collect32_tile(const CollectJob32 &J, int32_t k0
 
     const int rows = (m.n_points - b0) < kP ? (m.n_points - b0) : kP;
     const int n = rows * F;                        // words of this tile
-    if (J.dense) {
+    if (J.fs && !J.dense) {
+        // feature-major: 64 consecutive points of one feature per store wave
+        if (t < rows)
+            for (int f = 0; f < F; ++f)
+                stg1(J.dst + (int64_t)f * J.fs + b0 + t, tile[t * F + f]);
+    } else if (J.dense) {
         uint32_t *run = J.dst + (int64_t)b0 * F;   // 16-byte aligned: dst is, 64 * F is a multiple of 4
         for (int q = t; q < n / 4; q += kP)
             stg4(run + 4 * q, tile4[q]);
@@ -195,6 +200,7 @@ CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &
     j.n_tiles = (int32_t)((p.n_points + kP - 1) / kP);
     j.dense = ld == F && ((uintptr_t)dst & 15u) == 0;
     j.xcd = !p.pointwise;
+    j.fs = 0;
     return j;
 }
 

@@ -48,6 +48,7 @@ struct CollectJob32 {
     int32_t n_tiles;     // 64-point tiles
     int32_t dense;       // ld == F and a 16-byte aligned record: one contiguous run per tile
     int32_t xcd;         // XCD-contiguous tile order (maps with windows)
+    int64_t fs;          // 0: dst[p * ld + f]; else feature-major dst[f * fs + p] (ld unused)
 };
 CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &tab, uint32_t *dst, int64_t ld);
 // One launch for one or two jobs (n_jobs in {1, 2}).

@@ -184,7 +184,7 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
     //      unused values are replaced when stored), so all of them are in
     //      flight before the first use; only the dimensions where the wave
     //      touches an edge get a boundary fix-up.  The loads of tile t+1 are
-    //      issued before the output layer of tile t and land in registers.
+    //      issued after the first layer of tile t and land in registers.
     constexpr int PASSES = (G::T * 2 * KS1MAX + kThreads - 1) / kThreads;
     const int gp = tid % G::T;                     // this thread's point in a tile
     float gv[PASSES][8];
@@ -299,6 +299,12 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
             __syncthreads();               // the layer's activations are complete
         };
 
+        // the next tile's gather loads (the last tile re-reads itself, so the
+        // issue is unconditional) land during the hidden layers, the last
+        // epilogue and the output layer: windowed maps read neighbouring rows
+        // and planes that often miss the L2, and a shorter lead left part of
+        // that latency exposed
+        gather_issue(tile + nb < n_tiles ? tile + nb : tile);
         uint4 A[4][2];
         for (int h = 0; h < pk.n_hidden; ++h) {
             const uint32_t wbase = (uint32_t)((pk.off_wh + (int64_t)h * KT * G::NMB * 64) * 16);
@@ -340,10 +346,6 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                 __builtin_amdgcn_sched_barrier(0);
             }
         }
-        // the next tile's gather loads (the last tile re-reads itself, so the
-        // issue is unconditional) land while the last epilogue and the output
-        // layer run
-        gather_issue(tile + nb < n_tiles ? tile + nb : tile);
         load_a1();
         epilogue(pk.n_hidden);
 

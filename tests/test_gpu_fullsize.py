@@ -84,3 +84,27 @@ def test_cnn_fullsize(name):
     Y = oracle.cnn(w.model, oracle.gather(w.in_spec, w.inputs))
     worst, norm = assert_close(got, Y, RTOL["f32"], "%s full via %s" % (name, var))
     print("%s full [%s]: worst scaled %.3e, normwise %.3e" % (name, var, worst, norm))
+
+
+@pytest.mark.parametrize("name", ["stencil2d", "stencil3d"])
+def test_inplace_step_fullsize_sampled(name):
+    """One step written back into the fields it reads, at full size: the
+    snapshot record (feature-major, 18.8 GB for the 512^3 grid) keeps the
+    32-bit fused kernels; sampled outputs against the oracle's region on the
+    original fields."""
+    import torch
+    w = full(name)
+    fields = [torch.from_numpy(a).cuda() for a in w.inputs]
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.Model(w.model)
+    var = api.variant(m, mi, mo)
+    assert var.startswith("snapshot+mlp_" + w.compute), var
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    rows = wl.sample_rows(w.n_points, 2048, must=edges(w))
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model, rows)
+    gotY = np.stack([f.reshape(-1)[torch.from_numpy(rows).cuda()].cpu().numpy() for f in fields], 1)
+    worst, norm = assert_close(gotY, Y, RTOL[w.compute], "%s in place via %s" % (name, var))
+    print("%s in place [%s] full size: worst %.3e normwise %.3e" % (name, var, worst, norm))
+    del mi, mo, m
