@@ -243,6 +243,23 @@ def test_infer_nan_inputs_follow_relu(name):
     assert_close(gotY, expY, RTOL[w.compute], "%s via %s" % (name, var))
 
 
+@pytest.mark.parametrize("shape", [(9, 5, 256), (3, 2, 128)])
+def test_stencil3d_plane_order_visit(shape):
+    """Rows made of whole 128-point tiles: the bf16 kernel visits tiles with
+    the plane index fastest; every cell must still be written exactly as the
+    oracle's region writes it."""
+    w = wl.make("stencil3d", shape)
+    got, var = run_infer(w)
+    assert var.startswith("mlp_bf16_h512"), var
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    exp = [o.copy() for o in w.outputs]
+    oracle.scatter(w.out_spec, exp, Y)
+    assert_close(np.stack([a.reshape(-1) for a in got], 1), np.stack([a.reshape(-1) for a in exp], 1),
+                 RTOL["bf16"], "stencil3d %s via %s" % (shape, var))
+    for a in got:
+        assert not np.any(a.view(np.uint32) == wl.SENTINEL_BITS)
+
+
 def test_infer_fast_paths_are_used():
     for name, want in [("options", "mlp_f32_h64"), ("bonds", "mlp_f32_h128"), ("stencil2d", "mlp_f32_h128"),
                        ("poses", "mlp_bf16_h256"), ("stencil3d", "mlp_bf16_h512")]:
