@@ -172,57 +172,57 @@ __device__ __forceinline__ void conv_pass(const FusedArgs &a, const TabLds &tab,
             }
             off[j] = (ry * sw + rx) * CI;
         }
-        float acc[kPix][CO];
-#pragma unroll
-        for (int co = 0; co < CO; ++co) {
-            const float bv = bl[co];
-#pragma unroll
-            for (int j = 0; j < kPix; ++j)
-                acc[j][co] = bv;
-        }
-        // steps q = (kx, channel group) along a window row: the window values
-        // sit at 4q floats past the row's start and the packed weights
-        // ([ky][kx][ci][co]) at 4q * CO, so one step holds at most 64 weights
-        // in scalar registers whatever the channel counts
+        // output channels in groups of 4, one group at a time: a step (kx,
+        // 4 input channels) then holds 16 weights in scalar registers, which
+        // leaves the registers the pass's other uniform values need (larger
+        // weight sets spilled them); the window is re-read from LDS per group
         const int nq = kw * CIN4;
-        for (int ky = 0; ky < kh; ++ky) {
-            const float *wrow = wl + ky * nq * 4 * CO;
-            const int rowoff = ky * sw * CI;
-            for (int q = 0; q < nq; ++q) {
-                const float *wk = wrow + q * 4 * CO;
-                float4 v[kPix];
+#pragma unroll 1
+        for (int og = 0; og < COUT4; ++og) {
+            const float *wg = wl + og * kh * nq * 16;
+            float acc[kPix][4];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const float bv = bl[4 * og + c];
 #pragma unroll
                 for (int j = 0; j < kPix; ++j)
-                    v[j] = *reinterpret_cast<const float4 *>(src + off[j] + rowoff + 4 * q);
+                    acc[j][c] = bv;
+            }
+            for (int ky = 0; ky < kh; ++ky) {
+                const float *wrow = wg + ky * nq * 16;
+                const int rowoff = ky * sw * CI;
+                for (int q = 0; q < nq; ++q) {
+                    const float *wk = wrow + q * 16;
+                    float4 v[kPix];
 #pragma unroll
-                for (int ci = 0; ci < 4; ++ci)
+                    for (int j = 0; j < kPix; ++j)
+                        v[j] = *reinterpret_cast<const float4 *>(src + off[j] + rowoff + 4 * q);
 #pragma unroll
-                    for (int co = 0; co < CO; ++co) {
-                        const float wv = wk[ci * CO + co];
+                    for (int ci = 0; ci < 4; ++ci)
 #pragma unroll
-                        for (int j = 0; j < kPix; ++j) {
-                            const float x = ci == 0 ? v[j].x : ci == 1 ? v[j].y : ci == 2 ? v[j].z : v[j].w;
-                            acc[j][co] = fmaf(wv, x, acc[j][co]);
+                        for (int c = 0; c < 4; ++c) {
+                            const float wv = wk[ci * 4 + c];
+#pragma unroll
+                            for (int j = 0; j < kPix; ++j) {
+                                const float x = ci == 0 ? v[j].x : ci == 1 ? v[j].y : ci == 2 ? v[j].z : v[j].w;
+                                acc[j][c] = fmaf(wv, x, acc[j][c]);
+                            }
                         }
-                    }
+                }
             }
-        }
 #pragma unroll
-        for (int j = 0; j < kPix; ++j) {
-            if (Ly.act == HPACML_ACT_RELU) {
+            for (int j = 0; j < kPix; ++j) {
+                if (Ly.act == HPACML_ACT_RELU) {
 #pragma unroll
-                for (int co = 0; co < CO; ++co)
-                    acc[j][co] = relu_arith(acc[j][co]);
+                    for (int c = 0; c < 4; ++c)
+                        acc[j][c] = relu_arith(acc[j][c]);
+                }
+                if (!valid[j])
+                    continue;
+                const int i = base + j * kThreads + (int)threadIdx.x;
+                reinterpret_cast<float4 *>(dst + (size_t)i * CO)[og] =
+                    zero[j] ? make_float4(0.f, 0.f, 0.f, 0.f) : make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
             }
-            if (!valid[j])
-                continue;
-            const int i = base + j * kThreads + (int)threadIdx.x;
-            float4 *d4 = reinterpret_cast<float4 *>(dst + (size_t)i * CO);
-#pragma unroll
-            for (int c4 = 0; c4 < COUT4; ++c4)
-                d4[c4] = zero[j] ? make_float4(0.f, 0.f, 0.f, 0.f)
-                                 : make_float4(acc[j][4 * c4], acc[j][4 * c4 + 1], acc[j][4 * c4 + 2],
-                                               acc[j][4 * c4 + 3]);
         }
     }
 }
@@ -546,14 +546,14 @@ void cnn_fused_pack(const CnnPlan &p, const float *const *W, const float *const 
         d.act = y.act;
         d.mode = y.pad_mode;
         const int CI = 4 * d.cin4, CO = 4 * d.cout4;
-        // [ky][kx][ci][co], zero in the padded channels
+        // [co / 4][ky][kx][ci][co % 4], zero in the padded channels
         d.woff = (int32_t)buf.size();
         buf.resize(buf.size() + (size_t)d.kh * d.kw * CI * CO, 0.f);
         for (int co = 0; co < cout; ++co)
             for (int ci = 0; ci < cin; ++ci)
                 for (int ky = 0; ky < d.kh; ++ky)
                     for (int kx = 0; kx < d.kw; ++kx)
-                        buf[d.woff + (((size_t)ky * d.kw + kx) * CI + ci) * CO + co] =
+                        buf[d.woff + ((((size_t)(co / 4) * d.kh + ky) * d.kw + kx) * CI + ci) * 4 + co % 4] =
                             W[l][(((size_t)co * cin + ci) * d.kh + ky) * d.kw + kx];
         d.boff = (int32_t)buf.size();
         buf.resize(buf.size() + CO, 0.f);

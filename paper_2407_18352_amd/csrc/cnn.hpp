@@ -34,7 +34,7 @@ struct CnnFusedLayer {
 struct CnnFused {
     int32_t n_layers = 0, c0 = 0, cout_last = 0, circular = 0;
     CnnFusedLayer L[kCnnFusedMaxLayers]{};
-    const float *wts = nullptr;    // device: per layer [ky][kx][cin4*4][cout4*4], then bias [cout4*4]
+    const float *wts = nullptr;    // device: per layer [cout4][ky][kx][cin4*4][4], then bias [cout4*4]
 };
 bool cnn_fused_supported(const CnnPlan &p);
 // Packs the host weights; `out.wts` is left for the caller to set.
