@@ -86,6 +86,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="bonds", choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph-calls", type=int, default=0,
+                    help="also time N inference calls captured in one HIP graph and replayed (no per-call "
+                         "launch gaps), reported under graph_replay")
     ap.add_argument("--inplace", action="store_true",
                     help="write the outputs back into the input fields (a time step advanced in place: windowed "
                          "maps then run the snapshot pass); no oracle leg, the fields change every step")
@@ -218,6 +221,32 @@ def main():
                              "kernels": "hpacml_collect_pair: the input map's and the output map's records"},
         "wall_s_timed": wall,
     }
+
+    if args.graph_calls > 0:
+        # N back-to-back hpacml_infer calls captured once on a side stream and
+        # replayed: the kernel's throughput without host launch gaps
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            api.infer(model, mi, mo, side)          # outside capture: any lazy set-up happens here
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=side):
+                for _ in range(args.graph_calls):
+                    api.infer(model, mi, mo, side)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        per_call = e0.elapsed_time(e1) / args.graph_calls
+        result["graph_replay"] = {"calls": args.graph_calls, "ms_per_call": per_call,
+                                  "points_per_s": B / (per_call * 1e-3),
+                                  "achieved_tflops": flop_launch / (per_call * 1e-3) / 1e12,
+                                  "frac": flop_launch / (per_call * 1e-3) / peak}
 
     if not args.no_cpu_baseline and is_cnn:
         import oracle

@@ -566,3 +566,53 @@ def test_inplace_window_update_general_maps():
     got = np.stack([f.cpu().numpy().reshape(-1) for f in fields], 1)
     want = np.stack([a.reshape(-1) for a in exp], 1)
     assert_close(got, want, RTOL["f32"], "general in place via " + var)
+
+
+@pytest.mark.parametrize("case", ["options", "stencil3d", "inplace_stencil2d", "weather_cnn"])
+def test_graph_captured_inference_replays(case):
+    """hpacml_infer captured in a HIP graph and
+    replayed several times, with eager work and synchronisations between the
+    replays: every replay's outputs equal the eager call's bit for bit."""
+    import torch
+    if case == "weather_cnn":
+        w = wl.make_cnn("weather_cnn", (40, 130))
+        model = api.CnnModel(w.model)
+    else:
+        w = wl.make({"inplace_stencil2d": "stencil2d"}.get(case, case),
+                    {"options": 5000, "stencil3d": (6, 7, 9), "inplace_stencil2d": (20, 40)}[case])
+        model = api.Model(w.model)
+    ins = to_dev(w.inputs)
+    inplace = case.startswith("inplace")
+    outs = ins if inplace else to_dev(w.outputs)
+    mi = api.Map(w.in_spec, ins, _abi.TO)
+    mo = api.Map(w.out_spec, outs, _abi.FROM)
+    side = torch.cuda.Stream()
+
+    def reset():
+        for t, a in zip(ins, w.inputs):
+            t.copy_(torch.from_numpy(a))
+        if not inplace:
+            for t, a in zip(outs, w.outputs):
+                t.copy_(torch.from_numpy(a))
+        torch.cuda.synchronize()
+
+    # eager reference: one call (in place: one step from the original fields)
+    reset()
+    with torch.cuda.stream(side):
+        api.infer(model, mi, mo, side)
+    torch.cuda.synchronize()
+    want = [t.cpu().numpy().copy() for t in outs]
+    # capture: lazy set-up (the snapshot record) already happened in the eager call
+    g = torch.cuda.CUDAGraph()
+    reset()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            api.infer(model, mi, mo, side)
+    for k in range(4):
+        reset()
+        scratch = torch.randn(1 << 16, device="cuda")
+        (scratch * 2).sum().item()                      # eager work between replays
+        g.replay()
+        torch.cuda.synchronize()
+        for a, t in zip(want, outs):
+            assert np.array_equal(a.view(np.uint32), t.cpu().numpy().view(np.uint32)), (case, k)
