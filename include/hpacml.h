@@ -18,8 +18,14 @@
  * and every check is done on the host before anything is enqueued, so a call
  * that fails writes nothing.  `*out` handles are set to NULL on failure.
  *
- * Thread safety: handles are immutable after creation.  Concurrent infer and
- * collect calls with the same handles on different streams are allowed.
+ * Thread safety: maps and models are immutable after creation, except for
+ * two buffers allocated on first need and reused: a `to` map's snapshot
+ * record (inferences whose outputs overlap their inputs) and a convolutional
+ * model's workspace (its layer-by-layer path).  Concurrent infer and collect
+ * calls with the same handles on different streams are allowed, except that
+ * calls using one of those buffers must not overlap in time.  A region is
+ * used from one thread at a time, and its accurate path must not call
+ * functions of the same region.
  */
 #ifndef HPACML_H
 #define HPACML_H
