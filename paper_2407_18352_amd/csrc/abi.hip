@@ -696,16 +696,25 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
     if (cnn_use_fused(model, in, out))
         return hip_status(launch_cnn_fused(in->m32, out->m32, in->tab_dev, out->tab_dev, model->fused, (int32_t)S,
                                            c.height, c.width, st));
-    // layer by layer: gather every input into the workspace first, so the
-    // outputs may overwrite inputs
+    // layer by layer: the first layer reads the map's tensor (the input
+    // array itself when the map is a plain row-major view of it, else a
+    // gathered copy in the workspace); the outputs are scattered after the
+    // last layer, so they may overwrite inputs
     hpacml_model *mm = const_cast<hpacml_model *>(model);
     const int64_t per = S * c.max_elems;
-    float *a = nullptr, *b = nullptr;
+    // split-K partial sums of the fully connected layers
+    int64_t part_floats = 0;
+    for (const CnnLayerDev &L : model->cnn_layers) {
+        const int z = linear_splits(L, S);
+        if (z > 1)
+            part_floats = std::max<int64_t>(part_floats, (int64_t)z * S * L.cout);
+    }
+    float *a = nullptr, *b = nullptr, *part = nullptr;
     {
         std::lock_guard<std::mutex> lock(mm->ws_mu);
-        if (mm->ws_floats < 2 * per) {
+        if (mm->ws_floats < 2 * per + part_floats) {
             float *buf = nullptr;
-            hipError_t e = hipMalloc((void **)&buf, (size_t)(2 * per) * sizeof(float));
+            hipError_t e = hipMalloc((void **)&buf, (size_t)(2 * per + part_floats) * sizeof(float));
             if (e != hipSuccess) {
                 (void)hipGetLastError();
                 return hip_status(e);
@@ -714,23 +723,30 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
             e = hipStreamSynchronize(st);
             (void)hipFree(mm->ws);
             mm->ws = buf;
-            mm->ws_floats = 2 * per;
+            mm->ws_floats = 2 * per + part_floats;
             if (e != hipSuccess)
                 return hip_status(e);
         }
         a = mm->ws;
         b = mm->ws + per;
+        part = mm->ws + 2 * per;
     }
-    hpacml_status s = hpacml_collect(in, a, c.in_channels, st);
-    if (s != HPACML_OK)
-        return s;
+    const float *x = a;
+    if (in->plan.record_view) {
+        x = (const float *)in->plan.base[0];
+    } else {
+        hpacml_status s = hpacml_collect(in, a, c.in_channels, st);
+        if (s != HPACML_OK)
+            return s;
+    }
     for (int l = 0; l < c.n_layers; ++l) {
-        hipError_t e = launch_cnn_layer(model->cnn_layers[l], a, b, S, st);
+        hipError_t e = launch_cnn_layer(model->cnn_layers[l], x, b, S, part, st);
         if (e != hipSuccess)
             return hip_status(e);
+        x = b;
         std::swap(a, b);
     }
-    return hip_status(launch_scatter_record(out->dev, a, st));
+    return hip_status(launch_scatter_record(out->dev, x, st));
 }
 
 }  // namespace

@@ -370,6 +370,24 @@ __global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, const floa
 #pragma unroll
     for (int g = 0; g < kConvG; ++g)
         acc[g] = g < ng ? L.b[co0 + g] : 0.f;
+    if (!L.same) {
+        // VALID: every tap is inside the image
+        for (int ky = 0; ky < L.kh; ++ky) {
+            const float *prow = img + ((int64_t)(y0 + ky) * L.w + x0) * L.cin;
+            const float *wrow = L.W + (int64_t)co0 * wstride + ky * L.kw;
+            for (int kx = 0; kx < L.kw; ++kx) {
+                const float *px = prow + (int64_t)kx * L.cin;
+                const float *wk = wrow + kx;
+                for (int ci = 0; ci < L.cin; ++ci) {
+                    const float v = px[ci];
+#pragma unroll
+                    for (int g = 0; g < kConvG; ++g)
+                        if (g < ng)
+                            acc[g] = fmaf(wk[g * wstride + (int64_t)ci * L.kh * L.kw], v, acc[g]);
+                }
+            }
+        }
+    } else
     for (int ky = 0; ky < L.kh; ++ky) {
         int y = y0 + ky;
         bool zy = false;
@@ -436,9 +454,13 @@ __global__ void __launch_bounds__(256) cnn_pool_kernel(CnnLayerDev L, const floa
 // owns a T x T output tile (T = 64: 4 x 4 outputs per thread; T = 16 for
 // small layers, one output per thread, so that the grid still covers the
 // chip), K in chunks staged in LDS k-major, coalesced loads along k.
+// Split-K: block z of gridDim.z sums k in [z Kc, (z+1) Kc) and, when
+// gridDim.z > 1, writes its raw partial sums to part[z][S][O] (a reduce kernel
+// adds them in z order, then bias and activation).
 template <int T>
 __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const float *__restrict__ in,
-                                                        float *__restrict__ out, int64_t S) {
+                                                        float *__restrict__ out, int64_t S, int64_t Kc,
+                                                        float *__restrict__ part) {
     constexpr int R = T / 16;                 // outputs per thread per dimension
     constexpr int KC = 256 * 4 / T;           // k per chunk: each thread loads 4 values per operand
     __shared__ float xs[KC][T + 4];
@@ -449,8 +471,10 @@ __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const fl
     const int O = L.cout;
     const int64_t K = (int64_t)L.h * L.w * L.cin;
     const int ti = t / 16, tj = t % 16;
+    const int64_t kb = (int64_t)blockIdx.z * Kc;
+    const int64_t ke = kb + Kc < K ? kb + Kc : K;
     float acc[R][R] = {};
-    for (int64_t k0 = 0; k0 < K; k0 += KC) {
+    for (int64_t k0 = kb; k0 < ke; k0 += KC) {
         // T rows x KC columns of each operand: thread t loads column t % KC of
         // rows t / KC + (256 / KC) m
         const int c = t % KC;
@@ -460,8 +484,8 @@ __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const fl
             const int r = t / KC + (256 / KC) * m;
             const int64_t sr = s0 + r;
             const int o = o0 + r;
-            xs[c][r] = (sr < S && k < K) ? in[sr * K + k] : 0.f;
-            ws[c][r] = (o < O && k < K) ? L.W[(int64_t)o * K + k] : 0.f;
+            xs[c][r] = (sr < S && k < ke) ? in[sr * K + k] : 0.f;
+            ws[c][r] = (o < O && k < ke) ? L.W[(int64_t)o * K + k] : 0.f;
         }
         __syncthreads();
 #pragma unroll 8
@@ -489,11 +513,28 @@ __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const fl
         for (int j = 0; j < R; ++j) {
             const int o = o0 + R * tj + j;
             if (o < O) {
-                const float v = acc[i][j] + L.b[o];
-                out[sr * O + o] = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
+                if (gridDim.z > 1) {
+                    part[((int64_t)blockIdx.z * S + sr) * O + o] = acc[i][j];
+                } else {
+                    const float v = acc[i][j] + L.b[o];
+                    out[sr * O + o] = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
+                }
             }
         }
     }
+}
+
+__global__ void __launch_bounds__(256) cnn_linear_reduce_kernel(CnnLayerDev L, const float *__restrict__ part,
+                                                               float *__restrict__ out, int64_t S, int splits) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t n = S * L.cout;
+    if (idx >= n)
+        return;
+    float v = 0.f;
+    for (int z = 0; z < splits; ++z)
+        v += part[z * n + idx];
+    v += L.b[idx % L.cout];
+    out[idx] = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
 }
 
 __global__ void __launch_bounds__(256) scatter_record_kernel(DevMap m, const float *__restrict__ src) {
@@ -630,7 +671,20 @@ hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32
     return hipGetLastError();
 }
 
-hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, hipStream_t stream) {
+int linear_splits(const CnnLayerDev &L, int64_t S) {
+    if (L.kind != HPACML_LAYER_LINEAR)
+        return 1;
+    const int64_t K = (int64_t)L.h * L.w * L.cin;
+    const bool big = ((S + 63) / 64) * ((L.cout + 63) / 64) >= 512;
+    const int64_t T = big ? 64 : 16;
+    const int64_t blocks = ((S + T - 1) / T) * ((L.cout + T - 1) / T);
+    int64_t z = (1024 + blocks - 1) / blocks;                  // about 1024 blocks in all
+    z = std::min<int64_t>(z, std::max<int64_t>(1, K / 256));  // at least 256 k per block
+    return (int)std::max<int64_t>(1, std::min<int64_t>(z, kLinSplit));
+}
+
+hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
+                            hipStream_t stream) {
     const int64_t total = S * (int64_t)L.h2 * L.w2 * L.cout;
     if (total == 0)
         return hipSuccess;
@@ -652,17 +706,30 @@ hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, i
         break;
     default: {
         // 64 x 64 tiles when they still give two blocks per CU, else 16 x 16
+        // tiles, with K split over up to kLinSplit blocks when the tiles alone
+        // leave the chip short of blocks
         const bool big = ((S + 63) / 64) * ((L.cout + 63) / 64) >= 512;
         const int T = big ? 64 : 16;
         const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
         if (bx > INT32_MAX || by > 65535)
             return hipErrorInvalidValue;
+        const int64_t K = (int64_t)L.h * L.w * L.cin;
+        const int splits = linear_splits(L, S);
+        const int64_t Kc = (K + splits - 1) / splits;
         if (big)
-            hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, in,
-                               out, S);
+            hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by, splits), dim3(256), 0, stream,
+                               L, in, out, S, Kc, part);
         else
-            hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, in,
-                               out, S);
+            hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by, splits), dim3(256), 0, stream,
+                               L, in, out, S, Kc, part);
+        if (splits > 1) {
+            hipError_t e = hipGetLastError();
+            if (e != hipSuccess)
+                return e;
+            const int64_t n = S * L.cout;
+            hipLaunchKernelGGL(cnn_linear_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream, L,
+                               part, out, S, splits);
+        }
         break;
     }
     }

@@ -16,7 +16,12 @@ struct CnnLayerDev {
     int32_t h, w, h2, w2;          // input and output image sizes
     const float *W, *b;            // device, the caller's layouts
 };
-hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, hipStream_t stream);
+// `part`: scratch of linear_splits(L, S) * S * cout floats for a fully
+// connected layer whose K is split over several blocks (unused otherwise)
+constexpr int kLinSplit = 16;
+int linear_splits(const CnnLayerDev &L, int64_t S);
+hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
+                            hipStream_t stream);
 // src[p * F + g] -> feature g of point p of the (FROM) map
 hipError_t launch_scatter_record(const DevMap &m, const float *src, hipStream_t stream);
 

@@ -31,8 +31,11 @@ __device__ __forceinline__ void stg1(uint32_t *p, uint32_t v) {
 }
 
 // idx / F for idx < 2^16 and F <= 256: with M = ceil(2^24 / F) the error term
-// idx * (M * F - 2^24) stays below 2^24, so the quotient is exact.
-__device__ __forceinline__ uint32_t div_small(uint32_t idx, uint32_t magic) { return (idx * magic) >> 24; }
+// idx * (M * F - 2^24) stays below 2^24, so the quotient is exact.  The
+// product idx * M reaches 2^40, hence 64 bits.
+__device__ __forceinline__ uint32_t div_small(uint32_t idx, uint32_t magic) {
+    return (uint32_t)(((uint64_t)idx * magic) >> 24);
+}
 
 template <bool DENSE>
 __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__restrict__ dst, int64_t ld,
@@ -102,19 +105,25 @@ __global__ void __launch_bounds__(256) collect_kernel(DevMap m, uint32_t *__rest
 }
 
 // 32-bit form: Map32 view, feature table in the kernel arguments, one tile
-// of 64 points per block (no block loops over tiles), and boundary resolution
-// only along the dimensions where the wave touches an edge.  One launch
-// serves one or two maps (a region's input and output records): the first
-// jobs[0].n_tiles blocks take map 0, the rest map 1.
+// of U x 64 points per block of one wave (no block loops over tiles), and
+// boundary resolution only along the dimensions where the wave touches an
+// edge.  Maps with few features take several points per lane (U > 1), so a
+// block still moves a few KB and keeps several loads per lane in flight.
+// One launch serves one or two maps (a region's input and output records):
+// the first jobs[0].n_tiles blocks take map 0, the rest map 1.
 //
 // Tile order within a job: blocks of one XCD (blockIdx % 8) take a
 // contiguous range of tiles (windowed maps share halo lines in that XCD's
 // L2; consecutive tiles write consecutive record runs).
-constexpr int kP = 64;   // points per tile (one wave)
+constexpr int kP = 64;   // lanes per block (one wave)
+
+// points per lane for a map of F features: about 8 values per lane
+int32_t points_per_lane(int F) { return F == 1 ? 8 : F == 2 ? 4 : F <= 4 ? 2 : 1; }
 
 // (inlined once per job so that every field is read straight from the
 // kernel arguments: selecting between the two by reference would copy both
 // into private memory)
+template <int U>
 __device__ __forceinline__ void collect32_tile(const CollectJob32 &J, int32_t k0, u32x4 *tile4) {
     uint32_t *tile = reinterpret_cast<uint32_t *>(tile4);
     const Map32 &m = J.m;
@@ -127,45 +136,66 @@ __device__ __forceinline__ void collect32_tile(const CollectJob32 &J, int32_t k0
         const int32_t xq = n_tiles / 8, xr = n_tiles % 8, xx = k0 % 8;
         tileno = xx * xq + (xx < xr ? xx : xr) + k0 / 8;
     }
-    const int32_t b0 = tileno * kP;
-    const int32_t b = b0 + t;
-    const Pt32 pt = locate32(m, b < m.n_points ? b : m.n_points - 1);
-    const uint32_t edge = edge_dims32(m, pt);
+    constexpr int P = kP * U;                      // points per tile
+    const int32_t b0 = tileno * P;
+    // lane t takes the points b0 + t + 64 u
+    Pt32 pt[U];
+    uint32_t edge[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int64_t b = (int64_t)b0 + u * kP + t;   // b0 < n_points < 2^31; b may pass it
+        pt[u] = locate32(m, b < m.n_points ? (int32_t)b : m.n_points - 1);
+        edge[u] = edge_dims32(m, pt[u]);
+    }
 
-    // batches of K features: table entries fb..fb+K-1 exist (fb + K <= 64)
-    auto batch = [&](int fb, auto kb) {
-        constexpr int K = decltype(kb)::value;
-        uint32_t v[K];
-        if (edge == 0) {
+    if (U == 1) {
+        // batches of K features: table entries fb..fb+K-1 exist (fb + K <= 64)
+        auto batch = [&](int fb, auto kb) {
+            constexpr int K = decltype(kb)::value;
+            uint32_t v[K];
+            if (edge[0] == 0) {
+#pragma unroll
+                for (int e = 0; e < K; ++e)
+                    v[e] = ldg_bits(c.fptr[fb + e] + pt[0].pe);
+            } else {
+#pragma unroll
+                for (int e = 0; e < K; ++e)
+                    v[e] = ldg_bits(c.fptr[fb + e] + (pt[0].pe + edge_fix32(m, pt[0], c.raw8[fb + e], edge[0])));
+            }
 #pragma unroll
             for (int e = 0; e < K; ++e)
-                v[e] = ldg_bits(c.fptr[fb + e] + pt.pe);
-        } else {
+                if (fb + e < F)
+                    tile[t * F + fb + e] = v[e];
+        };
+        int fb = 0;
+        for (; fb + 8 <= F; fb += 8)
+            batch(fb, std::integral_constant<int, 8>{});
+        for (; fb < F; fb += 4)
+            batch(fb, std::integral_constant<int, 4>{});
+    } else {
+        // F <= 4: one feature at a time, U points per lane in flight
+        for (int f = 0; f < F; ++f) {
+            uint32_t v[U];
 #pragma unroll
-            for (int e = 0; e < K; ++e)
-                v[e] = ldg_bits(c.fptr[fb + e] + (pt.pe + edge_fix32(m, pt, c.raw8[fb + e], edge)));
+            for (int u = 0; u < U; ++u)
+                v[u] = ldg_bits(c.fptr[f] +
+                                (edge[u] ? pt[u].pe + edge_fix32(m, pt[u], c.raw8[f], edge[u]) : pt[u].pe));
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                tile[(u * kP + t) * F + f] = v[u];
         }
-#pragma unroll
-        for (int e = 0; e < K; ++e)
-            if (fb + e < F)
-                tile[t * F + fb + e] = v[e];
-    };
-    int fb = 0;
-    for (; fb + 8 <= F; fb += 8)
-        batch(fb, std::integral_constant<int, 8>{});
-    for (; fb < F; fb += 4)
-        batch(fb, std::integral_constant<int, 4>{});
+    }
     __syncthreads();
 
-    const int rows = (m.n_points - b0) < kP ? (m.n_points - b0) : kP;
+    const int rows = (m.n_points - b0) < P ? (m.n_points - b0) : P;
     const int n = rows * F;                        // words of this tile
     if (J.fs && !J.dense) {
         // feature-major: 64 consecutive points of one feature per store wave
-        if (t < rows)
+        for (int r = t; r < rows; r += kP)
             for (int f = 0; f < F; ++f)
-                stg1(J.dst + (int64_t)f * J.fs + b0 + t, tile[t * F + f]);
+                stg1(J.dst + (int64_t)f * J.fs + b0 + r, tile[r * F + f]);
     } else if (J.dense) {
-        uint32_t *run = J.dst + (int64_t)b0 * F;   // 16-byte aligned: dst is, 64 * F is a multiple of 4
+        uint32_t *run = J.dst + (int64_t)b0 * F;   // 16-byte aligned: dst is, P * F is a multiple of 4
         for (int q = t; q < n / 4; q += kP)
             stg4(run + 4 * q, tile4[q]);
         for (int i = (n & ~3) + t; i < n; i += kP)
@@ -179,12 +209,29 @@ __device__ __forceinline__ void collect32_tile(const CollectJob32 &J, int32_t k0
     }
 }
 
+__device__ __forceinline__ void collect32_job_tile(const CollectJob32 &J, int32_t k0, u32x4 *tile4) {
+    switch (J.ppl) {
+    case 8:
+        collect32_tile<8>(J, k0, tile4);
+        break;
+    case 4:
+        collect32_tile<4>(J, k0, tile4);
+        break;
+    case 2:
+        collect32_tile<2>(J, k0, tile4);
+        break;
+    default:
+        collect32_tile<1>(J, k0, tile4);
+        break;
+    }
+}
+
 __global__ void __launch_bounds__(kP) collect32_kernel(CollectJob32 j0, CollectJob32 j1) {
     extern __shared__ u32x4 tile4[];
     if ((int32_t)blockIdx.x < j0.n_tiles)
-        collect32_tile(j0, (int32_t)blockIdx.x, tile4);
+        collect32_job_tile(j0, (int32_t)blockIdx.x, tile4);
     else
-        collect32_tile(j1, (int32_t)blockIdx.x - j0.n_tiles, tile4);
+        collect32_job_tile(j1, (int32_t)blockIdx.x - j0.n_tiles, tile4);
 }
 
 }  // namespace
@@ -197,7 +244,8 @@ CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &
     j.ld = ld;
     const int F = p.n_features;
     j.magic = (uint32_t)(((1u << 24) + F - 1) / F);
-    j.n_tiles = (int32_t)((p.n_points + kP - 1) / kP);
+    j.ppl = points_per_lane(F);
+    j.n_tiles = (int32_t)((p.n_points + (int64_t)kP * j.ppl - 1) / ((int64_t)kP * j.ppl));
     j.dense = ld == F && ((uintptr_t)dst & 15u) == 0;
     j.xcd = !p.pointwise;
     j.fs = 0;
@@ -221,8 +269,9 @@ hipError_t launch_collect32(const CollectJob32 *jobs, int n_jobs, hipStream_t st
     const int64_t grid = (int64_t)j0.n_tiles + j1.n_tiles;
     if (grid == 0)
         return hipSuccess;
-    const int fmax = j0.m.n_features > j1.m.n_features ? j0.m.n_features : j1.m.n_features;
-    const size_t lds = (size_t)kP * fmax * sizeof(uint32_t);
+    // LDS tile: the larger of the two jobs' U x 64 x F words
+    const int w0 = j0.ppl * j0.m.n_features, w1 = j1.n_tiles ? j1.ppl * j1.m.n_features : 0;
+    const size_t lds = (size_t)kP * (w0 > w1 ? w0 : w1) * sizeof(uint32_t);
     hipLaunchKernelGGL(collect32_kernel, dim3((unsigned)grid), dim3(kP), lds, stream, j0, j1);
     return hipGetLastError();
 }

@@ -45,9 +45,10 @@ struct CollectJob32 {
     uint32_t *dst;
     int64_t ld;
     uint32_t magic;      // idx / F by multiply-shift (idx < 2^16)
-    int32_t n_tiles;     // 64-point tiles
+    int32_t n_tiles;     // tiles of ppl x 64 points
     int32_t dense;       // ld == F and a 16-byte aligned record: one contiguous run per tile
     int32_t xcd;         // XCD-contiguous tile order (maps with windows)
+    int32_t ppl;         // points per lane: 8, 4, 2 or 1 (F = 1, 2, 3-4, more)
     int64_t fs;          // 0: dst[p * ld + f]; else feature-major dst[f * fs + p] (ld unused)
 };
 CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &tab, uint32_t *dst, int64_t ld);

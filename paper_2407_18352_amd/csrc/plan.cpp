@@ -215,6 +215,29 @@ hpacml_status build_map_plan(const hpacml_functor *f, int32_t dir, const hpacml_
                 e.delta = delta;
             }
     }
+
+    // is the map's tensor [points][features] target 0's memory itself?  One
+    // target, every access inside the array (no boundary mode applies), the
+    // sweep's first point at element 0, feature f at element offset f, and
+    // the point strides those of a row-major [count...][F] array.
+    p.record_view = n_targets == 1 && npts > 0;
+    if (p.record_view) {
+        int64_t e0 = 0;
+        for (int d = 0; d < R; ++d) {
+            if (p.start[d] + p.omin[d] < 0 ||
+                p.start[d] + (p.count[d] - 1) * p.step[d] + p.omax[d] >= p.extent[d])
+                p.record_view = false;
+            e0 += p.start[d] * p.stride[d];
+        }
+        for (int fi = 0; p.record_view && fi < p.n_features; ++fi)
+            p.record_view = e0 + p.feat[fi].delta == fi;
+        int64_t want = p.n_features;
+        for (int d = R - 1; p.record_view && d >= 0; --d) {
+            if (p.count[d] > 1 && p.step[d] * p.stride[d] != want)
+                p.record_view = false;
+            want *= p.count[d];
+        }
+    }
     *out = std::move(p);
     return HPACML_OK;
 }

@@ -44,6 +44,9 @@ struct MapPlan {
     bool raw8 = false;        // every raw offset fits a signed byte and, along a
                               // periodic dimension, is at most the extent in size
                               // (one wrap resolves it)
+    bool record_view = false; // the tensor [points][features], row-major, is
+                              // target 0's memory: record element (b, f) is
+                              // base[0][b * n_features + f]
     std::vector<void *> base;             // [n_targets]
     std::vector<int64_t> stride;          // [n_targets * 4]
     std::vector<FeatureEntry> feat;       // [n_features]

@@ -142,6 +142,41 @@ def test_layered_path_stacks(case):
     _compare(got, _expected(w), "layered case %d" % case)
 
 
+@pytest.mark.parametrize("view", ["interleaved", "sweep_offset", "padded_rows"])
+def test_layered_input_read_in_place_or_gathered(view):
+    """Channels interleaved in one array [S][H][W*C] (a sweep of step C over
+    the last dimension, a slice of C elements): the map's tensor is then the
+    array itself, row for row, and the first layer reads it there; a sweep
+    that starts past the first frame, or rows padded past W*C, leave a
+    tensor that must be gathered first.  All three match the oracle.  The
+    1980-term fully connected sums are split over blocks with a ragged last
+    chunk."""
+    import torch
+    g = np.random.default_rng(4100 + ["interleaved", "sweep_offset", "padded_rows"].index(view))
+    S, H, W, C = 3, 24, 20, 2
+    layers = [wl.conv_layer(11, 0, C, 5, (3, 3), padding="valid"),
+              wl.linear_layer(12, 0, 22 * 18 * 5, 7), wl.linear_layer(13, 0, 7, 2, act=0)]
+    model = {"kind": "cnn", "in_channels": C, "image": (H, W), "layers": layers}
+    first = 1 if view == "sweep_offset" else 0
+    pad = 6 if view == "padded_rows" else 0
+    host = g.standard_normal((S + first, H, W * C + pad)).astype(np.float32)
+    host_view = host[:, :, :W * C]
+    spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, C))],
+            "sweep": ((first, 0, 0), (S + first, H, W * C), (1, 1, C)), "bnd": [0, 0, 0]}
+    dev = torch.from_numpy(host).cuda()
+    mi = api.Map(spec, [dev[:, :, :W * C]], _abi.TO)
+    outs = to_dev([wl.sentinel_like((S,)) for _ in range(2)])
+    mo = api.Map(wl.pointwise_spec(S), outs, _abi.FROM)
+    m = api.CnnModel(model)
+    assert api.variant(m, mi, mo) == "cnn_layers_f32"
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    exp = [wl.sentinel_like((S,)) for _ in range(2)]
+    oracle.infer(spec, [host_view], wl.pointwise_spec(S), exp, model)
+    _compare([o.cpu().numpy() for o in outs], exp, "first-layer input, %s" % view)
+    assert np.array_equal(dev.cpu().numpy().view(np.uint32), host.view(np.uint32))   # inputs untouched
+
+
 def test_window_map_channels_and_strided_views():
     """Channels from a 3x3 periodic window map (36 channels: layer by layer)
     and from column views of one array of structures (fused)."""

@@ -90,6 +90,44 @@ def test_collect_dense_and_offset_records(shape):
     m.close()
 
 
+@pytest.mark.parametrize("F", [1, 2, 3, 4])
+def test_collect_few_features_several_points_per_lane(F):
+    """Maps of 1-4 features take several points per lane: a periodic column
+    window of F elements (edges on both sides), a point count that leaves a
+    ragged last tile, dense, shifted and row-wise records, and one call that
+    pairs it with a map of another width."""
+    import torch
+    g = np.random.default_rng(60 + F)
+    ny, nx = 37, 71
+    a = g.standard_normal((ny, nx)).astype(np.float32)
+    spec = {"rank": 2, "slices": [((-1, 0), (F, 1))], "sweep": ((0, 0), (ny, nx), (1, 1)),
+            "bnd": [wl.PERIODIC, wl.CLAMP]}
+    want = oracle.collect(spec, [a])
+    dev = to_dev([a])
+    m = api.Map(spec, dev, _abi.TO)
+    n = m.n_points
+    assert m.n_features == F and n == ny * nx
+    rec = torch.empty(n * (F + 1) + 8, device="cuda", dtype=torch.int32)
+    for off, ld in ((0, F), (1, F), (0, F + 1)):
+        rec.fill_(-1)
+        api.collect(m, rec[off:off + n * ld].view(torch.float32), ld)
+        torch.cuda.synchronize()
+        got = rec.cpu().numpy().view(np.uint32)
+        body = got[off:off + n * ld].reshape(n, ld)
+        assert np.array_equal(body[:, :F], want), (off, ld)
+        assert np.all(body[:, F:] == 0xFFFFFFFF) and np.all(got[:off] == 0xFFFFFFFF), (off, ld)
+        assert np.all(got[off + n * ld:] == 0xFFFFFFFF), (off, ld)
+    # paired with a 3-feature pointwise map of another point count
+    b = [g.standard_normal(1234).astype(np.float32) for _ in range(3)]
+    mb = api.Map(wl.pointwise_spec(1234), to_dev(b), _abi.TO)
+    ra = torch.full((n, F), -1, device="cuda", dtype=torch.int32)
+    rb = torch.full((1234, 3), -1, device="cuda", dtype=torch.int32)
+    api.collect_pair(m, ra.view(torch.float32), F, mb, rb.view(torch.float32), 3)
+    torch.cuda.synchronize()
+    assert np.array_equal(ra.cpu().numpy().view(np.uint32), want)
+    assert np.array_equal(rb.cpu().numpy().view(np.uint32), oracle.collect(wl.pointwise_spec(1234), b))
+
+
 @pytest.mark.parametrize("name", wl.NAMES)
 def test_collect_pair_matches_two_collects(name):
     """Both records of a region in one call == the oracle's two records."""
@@ -517,6 +555,29 @@ def test_inplace_shifted_output_reads_snapshot():
     got = ins[0].cpu().numpy()
     assert got[0] == big[0][0]
     assert_close(got[1:, None], exp[0][1:, None], RTOL["f32"], "shifted in place via " + var)
+
+
+def test_inplace_three_fields_shifted_output_reads_snapshot():
+    """Three input fields (a feature-major snapshot record of three rows);
+    the output lands one element past the points of field 1."""
+    import torch
+    n = 1999
+    g = np.random.default_rng(71)
+    big = [g.uniform(-1, 1, n + 1).astype(np.float32) for _ in range(3)]
+    model = wl.make_model(5, [3, 64, 64, 1], "f32")
+    ins = to_dev(big)
+    spec = wl.pointwise_spec(n)
+    mi = api.Map(spec, [x[:n] for x in ins], _abi.TO)
+    mo = api.Map(spec, [ins[1][1:]], _abi.FROM)
+    m = api.Model(model)
+    var = api.variant(m, mi, mo)
+    assert var.startswith("snapshot+"), var
+    Y = oracle.infer_rows(spec, [x[:n] for x in big], model)
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    got = [x.cpu().numpy() for x in ins]
+    assert np.array_equal(got[0], big[0]) and np.array_equal(got[2], big[2]) and got[1][0] == big[1][0]
+    assert_close(got[1][1:, None], Y, RTOL["f32"], "three fields shifted in place via " + var)
 
 
 @pytest.mark.parametrize("name, size, steps", [("stencil2d", (20, 40), 2), ("stencil2d", (3, 130), 1),
