@@ -607,20 +607,20 @@ hpacml_status hpacml_cnn_create(int32_t in_channels, int32_t height, int32_t wid
             hpacml_model_destroy(m);
             return HPACML_E_DEVICE;
         }
-        // every layer's weights and biases in the caller's layouts
+        // every layer's weights and biases: convolutions packed for the
+        // layer kernel (32-byte aligned), fully connected layers in the
+        // caller's layout
         std::vector<float> host;
         std::vector<size_t> woff(n_layers), boff(n_layers);
         for (int l = 0; l < n_layers; ++l) {
             const hpacml_layer &y = layers[l];
             const CnnShape &si = p.shape[l], &so = p.shape[l + 1];
-            size_t nw = 0;
-            if (y.kind == HPACML_LAYER_CONV2D)
-                nw = (size_t)so.c * si.c * y.kernel[0] * y.kernel[1];
-            else if (y.kind == HPACML_LAYER_LINEAR)
-                nw = (size_t)so.c * si.h * si.w * si.c;
+            host.resize((host.size() + 7) / 8 * 8, 0.f);
             woff[l] = host.size();
-            if (nw)
-                host.insert(host.end(), W[l], W[l] + nw);
+            if (y.kind == HPACML_LAYER_CONV2D)
+                cnn_conv_pack(W[l], so.c, si.c, y.kernel[0], y.kernel[1], host);
+            else if (y.kind == HPACML_LAYER_LINEAR)
+                host.insert(host.end(), W[l], W[l] + (size_t)so.c * si.h * si.w * si.c);
             boff[l] = host.size();
             if (y.kind != HPACML_LAYER_MAXPOOL2D)
                 host.insert(host.end(), b[l], b[l] + so.c);
@@ -739,8 +739,24 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
         if (s != HPACML_OK)
             return s;
     }
+    const std::vector<CnnLayerDev> &ly = model->cnn_layers;
+    const int tail = cnn_tail_start(ly);
     for (int l = 0; l < c.n_layers; ++l) {
-        hipError_t e = launch_cnn_layer(model->cnn_layers[l], x, b, S, part, st);
+        hipError_t e;
+        if (l == tail) {
+            // the closing fully connected layers and the scatter
+            int splits = 1;
+            e = launch_cnn_linear_partials(ly[l], x, b, S, part, &splits, st);
+            if (e == hipSuccess)
+                e = launch_cnn_tail(ly, l, splits > 1 ? part : b, splits, out->dev, S, st);
+            return hip_status(e);
+        }
+        if (l + 1 < c.n_layers && cnn_pool_fusable(ly[l], ly[l + 1])) {
+            e = launch_cnn_conv(ly[l], &ly[l + 1], x, b, S, st);   // convolution + max-pool
+            ++l;
+        } else {
+            e = launch_cnn_layer(ly[l], x, b, S, part, st);
+        }
         if (e != hipSuccess)
             return hip_status(e);
         x = b;

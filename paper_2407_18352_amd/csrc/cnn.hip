@@ -348,84 +348,176 @@ constexpr size_t kLdsShared = 40 * 1024;
 constexpr size_t kLdsOneBlock = 160 * 1024;
 
 // ------------------------------------------------------------------ layers
-// One thread per output pixel and group of up to kConvG output channels
-// (the group is blockIdx.y, so the weights are wave-uniform scalar loads and
-// every input value read feeds kConvG FMAs).
-constexpr int kConvG = 8;
-__global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, const float *__restrict__ in,
-                                                      float *__restrict__ out, int64_t n_pix) {
-    const int64_t pix = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (pix >= n_pix)
-        return;
-    const int co0 = blockIdx.y * kConvG;
-    const int ng = min(kConvG, L.cout - co0);
-    const int ox = (int)(pix % L.w2);
-    const int oy = (int)(pix / L.w2 % L.h2);
-    const int64_t s = pix / ((int64_t)L.w2 * L.h2);
-    const float *img = in + s * L.h * L.w * L.cin;
+// One thread per output pixel and group of kConvG output channels
+// (blockIdx.y).  Weights packed [group][ky][kx][ci][kConvG], zero past cout:
+// in the channels-last image the taps of one window row are one contiguous
+// run of kw * cin floats, and the kConvG weights of a tap are one
+// wave-uniform 32-byte scalar load, so every input value read feeds kConvG
+// FMAs.  Taps go in chunks of kTapChunk whose input loads are all issued
+// before the first FMA.  A pixel whose window leaves the image (SAME
+// padding at the border) resolves each tap through the padding mode.
+//
+// With POOL, a max-pool whose windows do not overlap follows in the same
+// kernel, so the convolution's output never goes to memory: a group of
+// 2^qshift adjacent lanes holds one pooled pixel, lane q computing window
+// position q (lanes past the window repeat position 0), and the group's
+// maximum comes from xor shuffles.  Each pairwise step keeps the lower
+// lane's value unless the other is larger or a NaN, and a NaN once taken
+// stays: the window's first NaN, else its first maximum, as in the pool
+// kernel.
+constexpr int kTapChunk = 16;
+
+// Convolution outputs (bias, taps, activation) of output pixel (oy, ox).
+__device__ __forceinline__ void conv_pixel(const CnnLayerDev &L, const float *img, const float *__restrict__ wg,
+                                           int oy, int ox, int ng, float (&acc)[kConvG]) {
     const int y0 = oy * L.sh - (L.same ? (L.kh - 1) / 2 : 0);
     const int x0 = ox * L.sw - (L.same ? (L.kw - 1) / 2 : 0);
-    const int64_t wstride = (int64_t)L.cin * L.kh * L.kw;   // one output channel's weights
-    float acc[kConvG];
+    const int taps = L.kh * L.kw * L.cin;
 #pragma unroll
     for (int g = 0; g < kConvG; ++g)
-        acc[g] = g < ng ? L.b[co0 + g] : 0.f;
-    if (!L.same) {
-        // VALID: every tap is inside the image
+        acc[g] = g < ng ? L.b[blockIdx.y * kConvG + g] : 0.f;
+    if (y0 >= 0 && x0 >= 0 && y0 + L.kh <= L.h && x0 + L.kw <= L.w) {
+        const float *base = img + ((int64_t)y0 * L.w + x0) * L.cin;
+        const int run = L.kw * L.cin;                 // floats of one window row
+        const int64_t rs = (int64_t)L.w * L.cin;      // image row stride
+        int ky = 0, r = 0;
+        if (run % 4 == 0 && rs % 4 == 0 && ((uintptr_t)base & 15) == 0) {
+            // window rows of whole, aligned float4s: 16-byte loads
+            for (int t0 = 0; t0 < taps; t0 += kTapChunk) {
+                float4 v[kTapChunk / 4];
+#pragma unroll
+                for (int j = 0; j < kTapChunk / 4; ++j) {
+                    v[j] = t0 + 4 * j < taps ? *reinterpret_cast<const float4 *>(base + ky * rs + r)
+                                             : make_float4(0.f, 0.f, 0.f, 0.f);
+                    r += 4;
+                    if (r == run) {
+                        r = 0;
+                        ++ky;
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < kTapChunk / 4; ++j)
+                    if (t0 + 4 * j < taps) {
+                        const float *w = wg + (int64_t)(t0 + 4 * j) * kConvG;
+                        const float e[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+#pragma unroll
+                            for (int g = 0; g < kConvG; ++g)
+                                acc[g] = fmaf(w[i * kConvG + g], e[i], acc[g]);
+                    }
+            }
+        } else
+        for (int t0 = 0; t0 < taps; t0 += kTapChunk) {
+            float v[kTapChunk];
+#pragma unroll
+            for (int j = 0; j < kTapChunk; ++j) {
+                v[j] = t0 + j < taps ? base[ky * rs + r] : 0.f;
+                if (++r == run) {
+                    r = 0;
+                    ++ky;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kTapChunk; ++j)
+                if (t0 + j < taps) {
+                    const float *w = wg + (int64_t)(t0 + j) * kConvG;
+#pragma unroll
+                    for (int g = 0; g < kConvG; ++g)
+                        acc[g] = fmaf(w[g], v[j], acc[g]);
+                }
+        }
+    } else {
         for (int ky = 0; ky < L.kh; ++ky) {
-            const float *prow = img + ((int64_t)(y0 + ky) * L.w + x0) * L.cin;
-            const float *wrow = L.W + (int64_t)co0 * wstride + ky * L.kw;
+            int y = y0 + ky;
+            bool zy = false;
+            if (y < 0 || y >= L.h) {
+                if (L.mode == HPACML_PADMODE_CIRCULAR)
+                    y = wrap(y, L.h);
+                else if (L.mode == HPACML_PADMODE_REPLICATE)
+                    y = min(max(y, 0), L.h - 1);
+                else
+                    zy = true;
+            }
             for (int kx = 0; kx < L.kw; ++kx) {
-                const float *px = prow + (int64_t)kx * L.cin;
-                const float *wk = wrow + kx;
+                int x = x0 + kx;
+                bool z = zy;
+                if (x < 0 || x >= L.w) {
+                    if (L.mode == HPACML_PADMODE_CIRCULAR)
+                        x = wrap(x, L.w);
+                    else if (L.mode == HPACML_PADMODE_REPLICATE)
+                        x = min(max(x, 0), L.w - 1);
+                    else
+                        z = true;
+                }
+                if (z)
+                    continue;
+                const float *px = img + ((int64_t)y * L.w + x) * L.cin;
+                const float *wk = wg + (int64_t)(ky * L.kw + kx) * L.cin * kConvG;
                 for (int ci = 0; ci < L.cin; ++ci) {
                     const float v = px[ci];
 #pragma unroll
                     for (int g = 0; g < kConvG; ++g)
-                        if (g < ng)
-                            acc[g] = fmaf(wk[g * wstride + (int64_t)ci * L.kh * L.kw], v, acc[g]);
+                        acc[g] = fmaf(wk[ci * kConvG + g], v, acc[g]);
                 }
             }
         }
-    } else
-    for (int ky = 0; ky < L.kh; ++ky) {
-        int y = y0 + ky;
-        bool zy = false;
-        if (y < 0 || y >= L.h) {
-            if (L.mode == HPACML_PADMODE_CIRCULAR)
-                y = wrap(y, L.h);
-            else if (L.mode == HPACML_PADMODE_REPLICATE)
-                y = min(max(y, 0), L.h - 1);
-            else
-                zy = true;
-        }
-        for (int kx = 0; kx < L.kw; ++kx) {
-            int x = x0 + kx;
-            bool z = zy;
-            if (x < 0 || x >= L.w) {
-                if (L.mode == HPACML_PADMODE_CIRCULAR)
-                    x = wrap(x, L.w);
-                else if (L.mode == HPACML_PADMODE_REPLICATE)
-                    x = min(max(x, 0), L.w - 1);
-                else
-                    z = true;
-            }
-            if (z)
-                continue;
-            const float *px = img + ((int64_t)y * L.w + x) * L.cin;
-            const float *wk = L.W + (int64_t)co0 * wstride + ky * L.kw + kx;
-            for (int ci = 0; ci < L.cin; ++ci) {
-                const float v = px[ci];
+    }
 #pragma unroll
-                for (int g = 0; g < kConvG; ++g)
-                    if (g < ng)
-                        acc[g] = fmaf(wk[g * wstride + (int64_t)ci * L.kh * L.kw], v, acc[g]);
+    for (int g = 0; g < kConvG; ++g)
+        acc[g] = L.act == HPACML_ACT_RELU ? (acc[g] > 0.f ? acc[g] : 0.f) : acc[g];
+}
+
+template <bool POOL>
+__global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, CnnLayerDev P, int qshift,
+                                                      const float *__restrict__ in, float *__restrict__ out,
+                                                      int64_t n_pix) {
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t pix = POOL ? tid >> qshift : tid;
+    if (!POOL && pix >= n_pix)
+        return;
+    // (pooled: every lane of a group takes part in the shuffles)
+    const int64_t pc = pix < n_pix ? pix : n_pix - 1;
+    const int co0 = blockIdx.y * kConvG;
+    const int ng = min(kConvG, L.cout - co0);
+    const int W2 = POOL ? P.w2 : L.w2, H2 = POOL ? P.h2 : L.h2;
+    int ox = (int)(pc % W2);
+    int oy = (int)(pc / W2 % H2);
+    const int64_t s = pc / ((int64_t)W2 * H2);
+    const int q = POOL ? (int)(tid & ((1 << qshift) - 1)) : 0;
+    if (POOL) {
+        const int qq = q < P.kh * P.kw ? q : 0;
+        oy = oy * P.sh + qq / P.kw;
+        ox = ox * P.sw + qq % P.kw;
+    }
+    const float *img = in + s * L.h * L.w * L.cin;
+    const float *__restrict__ wg = L.W + (int64_t)blockIdx.y * L.kh * L.kw * L.cin * kConvG;
+    float acc[kConvG];
+    conv_pixel(L, img, wg, oy, ox, ng, acc);
+    if (POOL) {
+        for (int d = 1; d < (1 << qshift); d <<= 1) {
+            const bool lower = (q & d) == 0;
+#pragma unroll
+            for (int g = 0; g < kConvG; ++g) {
+                const float o = __shfl_xor(acc[g], d);
+                const float a = lower ? acc[g] : o, b = lower ? o : acc[g];
+                acc[g] = (!(a != a) && (b != b || b > a)) ? b : a;
             }
         }
+#pragma unroll
+        for (int g = 0; g < kConvG; ++g)
+            acc[g] = P.act == HPACML_ACT_RELU ? (acc[g] > 0.f ? acc[g] : 0.f) : acc[g];
+        if (q != 0 || pix >= n_pix)
+            return;
     }
     float *o = out + pix * L.cout + co0;
-    for (int g = 0; g < ng; ++g)
-        o[g] = L.act == HPACML_ACT_RELU ? (acc[g] > 0.f ? acc[g] : 0.f) : acc[g];
+    if (ng == kConvG && ((uintptr_t)o & 15) == 0) {
+        *reinterpret_cast<float4 *>(o) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+        *reinterpret_cast<float4 *>(o + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    } else {
+        for (int g = 0; g < ng; ++g)
+            o[g] = acc[g];
+    }
 }
 
 __global__ void __launch_bounds__(256) cnn_pool_kernel(CnnLayerDev L, const float *__restrict__ in,
@@ -452,8 +544,8 @@ __global__ void __launch_bounds__(256) cnn_pool_kernel(CnnLayerDev L, const floa
 
 // Fully connected layer over S images: out[S][O] = in[S][K] W^T + b.  A block
 // owns a T x T output tile (T = 64: 4 x 4 outputs per thread; T = 16 for
-// small layers, one output per thread, so that the grid still covers the
-// chip), K in chunks staged in LDS k-major, coalesced loads along k.
+// layers of at most 16 outputs, one output per thread), K in chunks staged in
+// LDS k-major, coalesced loads along k.
 // Split-K: block z of gridDim.z sums k in [z Kc, (z+1) Kc) and, when
 // gridDim.z > 1, writes its raw partial sums to part[z][S][O] (a reduce kernel
 // adds them in z order, then bias and activation).
@@ -474,20 +566,33 @@ __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const fl
     const int64_t kb = (int64_t)blockIdx.z * Kc;
     const int64_t ke = kb + Kc < K ? kb + Kc : K;
     float acc[R][R] = {};
-    for (int64_t k0 = kb; k0 < ke; k0 += KC) {
-        // T rows x KC columns of each operand: thread t loads column t % KC of
-        // rows t / KC + (256 / KC) m
-        const int c = t % KC;
+    // T rows x KC columns of each operand per chunk: thread t loads column
+    // t % KC of rows t / KC + (256 / KC) m, into registers one chunk ahead
+    const int c = t % KC;
+    float xr[4], wr[4];
+    auto fetch = [&](int64_t k0) {
         const int64_t k = k0 + c;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int r = t / KC + (256 / KC) * m;
             const int64_t sr = s0 + r;
             const int o = o0 + r;
-            xs[c][r] = (sr < S && k < ke) ? in[sr * K + k] : 0.f;
-            ws[c][r] = (o < O && k < ke) ? L.W[(int64_t)o * K + k] : 0.f;
+            xr[m] = (sr < S && k < ke) ? in[sr * K + k] : 0.f;
+            wr[m] = (o < O && k < ke) ? L.W[(int64_t)o * K + k] : 0.f;
+        }
+    };
+    if (kb < ke)
+        fetch(kb);
+    for (int64_t k0 = kb; k0 < ke; k0 += KC) {
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int r = t / KC + (256 / KC) * m;
+            xs[c][r] = xr[m];
+            ws[c][r] = wr[m];
         }
         __syncthreads();
+        if (k0 + KC < ke)
+            fetch(k0 + KC);
 #pragma unroll 8
         for (int kk = 0; kk < KC; ++kk) {
             float a[R], b[R];
@@ -531,10 +636,70 @@ __global__ void __launch_bounds__(256) cnn_linear_reduce_kernel(CnnLayerDev L, c
     if (idx >= n)
         return;
     float v = 0.f;
+#pragma unroll 8
     for (int z = 0; z < splits; ++z)
         v += part[z * n + idx];
     v += L.b[idx % L.cout];
     out[idx] = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
+}
+
+// The fully connected layers that end a stack, once the first of them has
+// run its products: a block of 256 threads takes 256 / width images (width =
+// the widest of these layers), adds the first layer's partial sums in block
+// order with bias and activation (or reads its finished outputs), runs the
+// remaining small layers on vectors in LDS (thread (image, o) computes
+// output o in k order, then adds the bias), and scatters the last layer's
+// outputs through the `from` map (one point per image).
+__global__ void __launch_bounds__(256) cnn_tail_kernel(CnnTail T, const float *__restrict__ src, DevMap m,
+                                                      int64_t S) {
+    __shared__ float buf[2][256];
+    const int ws = T.width;
+    const int sb = threadIdx.x / ws, o = threadIdx.x % ws;
+    const int64_t s = (int64_t)blockIdx.x * (256 / ws) + sb;
+    const bool live = sb < 256 / ws && s < S;
+    {
+        const CnnLayerDev &L = T.first;
+        if (live && o < L.cout) {
+            float v;
+            if (T.splits) {
+                const int64_t n = S * L.cout, idx = s * L.cout + o;
+                v = 0.f;
+#pragma unroll 8
+                for (int z = 0; z < T.splits; ++z)
+                    v += src[z * n + idx];
+                v += L.b[o];
+                v = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
+            } else {
+                v = src[s * L.cout + o];
+            }
+            buf[0][sb * ws + o] = v;
+        }
+    }
+    __syncthreads();
+    int cur = 0, width = T.first.cout;
+#pragma unroll
+    for (int l = 0; l < kTailLayers; ++l) {
+        if (l >= T.n_rest)
+            break;
+        const CnnLayerDev &L = T.rest[l];
+        if (live && o < L.cout) {
+            const float *h = &buf[cur][sb * ws];
+            const float *w = L.W + (int64_t)o * width;
+            float acc = 0.f;
+            for (int k = 0; k < width; ++k)
+                acc = fmaf(h[k], w[k], acc);
+            const float v = acc + L.b[o];
+            buf[cur ^ 1][sb * ws + o] = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
+        }
+        __syncthreads();
+        cur ^= 1;
+        width = L.cout;
+    }
+    if (live && o < width) {
+        int64_t p[HPACML_MAX_RANK];
+        sweep_point(m, s, p);
+        stg(const_cast<float *>(feature_ptr(m, p, interior(m, p), o)), buf[cur][sb * ws + o]);
+    }
 }
 
 __global__ void __launch_bounds__(256) scatter_record_kernel(DevMap m, const float *__restrict__ src) {
@@ -671,16 +836,59 @@ hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32
     return hipGetLastError();
 }
 
+void cnn_conv_pack(const float *W, int cout, int cin, int kh, int kw, std::vector<float> &dst) {
+    const int groups = (cout + kConvG - 1) / kConvG;
+    const size_t taps = (size_t)kh * kw * cin, at = dst.size();
+    dst.resize(at + groups * taps * kConvG, 0.f);
+    for (int co = 0; co < cout; ++co)
+        for (int ci = 0; ci < cin; ++ci)
+            for (int ky = 0; ky < kh; ++ky)
+                for (int kx = 0; kx < kw; ++kx)
+                    dst[at + ((co / kConvG) * taps + ((size_t)ky * kw + kx) * cin + ci) * kConvG + co % kConvG] =
+                        W[(((size_t)co * cin + ci) * kh + ky) * kw + kx];
+}
+
+// Output tile of a fully connected layer: 64 x 64 (4 x 4 outputs per thread,
+// two 16-byte LDS reads per 16 FMAs) unless the layer has at most 16
+// outputs, where most of such a tile would be padding.
+int linear_tile(const CnnLayerDev &L) { return L.cout > 16 ? 64 : 16; }
+
 int linear_splits(const CnnLayerDev &L, int64_t S) {
     if (L.kind != HPACML_LAYER_LINEAR)
         return 1;
     const int64_t K = (int64_t)L.h * L.w * L.cin;
-    const bool big = ((S + 63) / 64) * ((L.cout + 63) / 64) >= 512;
-    const int64_t T = big ? 64 : 16;
+    const int64_t T = linear_tile(L);
     const int64_t blocks = ((S + T - 1) / T) * ((L.cout + T - 1) / T);
-    int64_t z = (1024 + blocks - 1) / blocks;                  // about 1024 blocks in all
-    z = std::min<int64_t>(z, std::max<int64_t>(1, K / 256));  // at least 256 k per block
+    int64_t z = (512 + blocks - 1) / blocks;                   // about 512 blocks in all
+    z = std::min<int64_t>(z, std::max<int64_t>(1, K / 128));  // at least 128 k per block
     return (int)std::max<int64_t>(1, std::min<int64_t>(z, kLinSplit));
+}
+
+// pooled pixels take groups of 2^qshift lanes: windows of at most 16
+// positions, so that a group wastes at most 7 of 16 lanes
+bool cnn_pool_fusable(const CnnLayerDev &conv, const CnnLayerDev &pool) {
+    return conv.kind == HPACML_LAYER_CONV2D && pool.kind == HPACML_LAYER_MAXPOOL2D && pool.sh == pool.kh &&
+           pool.sw == pool.kw && pool.kh * pool.kw <= 16;
+}
+
+hipError_t launch_cnn_conv(const CnnLayerDev &L, const CnnLayerDev *pool, const float *in, float *out, int64_t S,
+                           hipStream_t stream) {
+    const int64_t n_pix = S * (pool ? (int64_t)pool->h2 * pool->w2 : (int64_t)L.h2 * L.w2);
+    if (n_pix == 0)
+        return hipSuccess;
+    int qshift = 0;
+    while (pool && (1 << qshift) < pool->kh * pool->kw)
+        ++qshift;
+    const int64_t bx = ((n_pix << qshift) + 255) / 256, by = (L.cout + kConvG - 1) / kConvG;
+    if (bx > INT32_MAX || by > 65535)
+        return hipErrorInvalidValue;
+    if (pool)
+        hipLaunchKernelGGL(cnn_conv_kernel<true>, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, *pool,
+                           qshift, in, out, n_pix);
+    else
+        hipLaunchKernelGGL(cnn_conv_kernel<false>, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, L, 0,
+                           in, out, n_pix);
+    return hipGetLastError();
 }
 
 hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
@@ -692,24 +900,16 @@ hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, i
     if (blocks > INT32_MAX)
         return hipErrorInvalidValue;
     switch (L.kind) {
-    case HPACML_LAYER_CONV2D: {
-        const int64_t n_pix = S * (int64_t)L.h2 * L.w2;
-        const int64_t bx = (n_pix + 255) / 256, by = (L.cout + kConvG - 1) / kConvG;
-        if (bx > INT32_MAX || by > 65535)
-            return hipErrorInvalidValue;
-        hipLaunchKernelGGL(cnn_conv_kernel, dim3((unsigned)bx, (unsigned)by), dim3(256), 0, stream, L, in, out,
-                           n_pix);
-        break;
-    }
+    case HPACML_LAYER_CONV2D:
+        return launch_cnn_conv(L, nullptr, in, out, S, stream);
     case HPACML_LAYER_MAXPOOL2D:
         hipLaunchKernelGGL(cnn_pool_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, L, in, out, total);
         break;
     default: {
-        // 64 x 64 tiles when they still give two blocks per CU, else 16 x 16
-        // tiles, with K split over up to kLinSplit blocks when the tiles alone
-        // leave the chip short of blocks
-        const bool big = ((S + 63) / 64) * ((L.cout + 63) / 64) >= 512;
-        const int T = big ? 64 : 16;
+        // K split over up to kLinSplit blocks when the tiles alone leave the
+        // chip short of blocks
+        const int T = linear_tile(L);
+        const bool big = T == 64;
         const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
         if (bx > INT32_MAX || by > 65535)
             return hipErrorInvalidValue;
@@ -733,6 +933,65 @@ hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, i
         break;
     }
     }
+    return hipGetLastError();
+}
+
+int cnn_tail_start(const std::vector<CnnLayerDev> &ly) {
+    const int n = (int)ly.size();
+    int t = n;
+    // the trailing fully connected layers whose inputs are at most 256 wide
+    while (t > 0 && ly[t - 1].kind == HPACML_LAYER_LINEAR && ly[t - 1].cout <= 256 &&
+           (int64_t)ly[t - 1].h * ly[t - 1].w * ly[t - 1].cin <= 256)
+        --t;
+    // the fully connected layer before them (any K) starts the tail
+    if (t > 0 && ly[t - 1].kind == HPACML_LAYER_LINEAR && ly[t - 1].cout <= 256)
+        --t;
+    if (t == n)
+        return -1;
+    return n - 1 - t <= kTailLayers ? t : -1;
+}
+
+hipError_t launch_cnn_tail(const std::vector<CnnLayerDev> &ly, int start, const float *src, int splits,
+                           const DevMap &out, int64_t S, hipStream_t stream) {
+    if (S == 0)
+        return hipSuccess;
+    CnnTail T{};
+    T.first = ly[start];
+    T.n_rest = (int)ly.size() - 1 - start;
+    T.splits = splits > 1 ? splits : 0;
+    int width = T.first.cout;
+    for (int l = 0; l < T.n_rest; ++l) {
+        T.rest[l] = ly[start + 1 + l];
+        width = std::max(width, T.rest[l].cout);
+    }
+    int ws = 1;
+    while (ws < width)
+        ws *= 2;
+    T.width = ws;
+    const int64_t per = 256 / ws, blocks = (S + per - 1) / per;
+    if (blocks > INT32_MAX)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(cnn_tail_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, T, src, out, S);
+    return hipGetLastError();
+}
+
+hipError_t launch_cnn_linear_partials(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
+                                      int *splits, hipStream_t stream) {
+    *splits = linear_splits(L, S);
+    if (*splits <= 1)
+        return launch_cnn_layer(L, in, out, S, part, stream);
+    const int T = linear_tile(L);
+    const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
+    if (bx > INT32_MAX || by > 65535)
+        return hipErrorInvalidValue;
+    const int64_t K = (int64_t)L.h * L.w * L.cin;
+    const int64_t Kc = (K + *splits - 1) / *splits;
+    if (T == 64)
+        hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by, *splits), dim3(256), 0, stream, L,
+                           in, out, S, Kc, part);
+    else
+        hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by, *splits), dim3(256), 0, stream, L,
+                           in, out, S, Kc, part);
     return hipGetLastError();
 }
 

@@ -11,17 +11,46 @@ namespace hpacml {
 
 // ---- layer-by-layer path: one kernel per layer over S images ([S][h][w][c]
 // tensors in a workspace), then a scatter of the last one.
+constexpr int kConvG = 8;           // output channels per convolution thread
 struct CnnLayerDev {
     int32_t kind, cin, cout, kh, kw, sh, sw, same, mode, act;
     int32_t h, w, h2, w2;          // input and output image sizes
-    const float *W, *b;            // device, the caller's layouts
+    const float *W, *b;            // device: convolution weights packed by
+                                   // cnn_conv_pack, else the caller's layouts
 };
+// Convolution weights [cout][cin][kh][kw] -> [ceil(cout / kConvG)][kh][kw][cin]
+// [kConvG], zero past cout (appended to `dst`).
+void cnn_conv_pack(const float *W, int cout, int cin, int kh, int kw, std::vector<float> &dst);
 // `part`: scratch of linear_splits(L, S) * S * cout floats for a fully
 // connected layer whose K is split over several blocks (unused otherwise)
-constexpr int kLinSplit = 16;
+constexpr int kLinSplit = 32;
 int linear_splits(const CnnLayerDev &L, int64_t S);
 hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
                             hipStream_t stream);
+// A convolution and the max-pool after it in one kernel: pools whose
+// windows do not overlap (stride == window).
+bool cnn_pool_fusable(const CnnLayerDev &conv, const CnnLayerDev &pool);
+hipError_t launch_cnn_conv(const CnnLayerDev &L, const CnnLayerDev *pool, const float *in, float *out, int64_t S,
+                           hipStream_t stream);
+// The fully connected layers that end a stack in one kernel with the
+// scatter: cnn_tail_start gives the first of them (any K, at most 256
+// outputs; the rest at most 256 wide, at most kTailLayers of them), or -1.
+// launch_cnn_linear_partials runs that first layer's products (raw split-K
+// partials, or finished outputs when *splits comes back 1); launch_cnn_tail
+// the rest.
+constexpr int kTailLayers = 4;
+struct CnnTail {
+    CnnLayerDev first;
+    CnnLayerDev rest[kTailLayers];
+    int32_t n_rest;
+    int32_t splits;                // 0: src holds the first layer's outputs [S][cout]
+    int32_t width;                 // power of two >= every layer's width
+};
+int cnn_tail_start(const std::vector<CnnLayerDev> &ly);
+hipError_t launch_cnn_linear_partials(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
+                                      int *splits, hipStream_t stream);
+hipError_t launch_cnn_tail(const std::vector<CnnLayerDev> &ly, int start, const float *src, int splits,
+                           const DevMap &out, int64_t S, hipStream_t stream);
 // src[p * F + g] -> feature g of point p of the (FROM) map
 hipError_t launch_scatter_record(const DevMap &m, const float *src, hipStream_t stream);
 

@@ -177,6 +177,70 @@ def test_layered_input_read_in_place_or_gathered(view):
     assert np.array_equal(dev.cpu().numpy().view(np.uint32), host.view(np.uint32))   # inputs untouched
 
 
+@pytest.mark.parametrize("pool_k", [(2, 2), (3, 3), (1, 3), (4, 4)])
+def test_conv_then_pool_in_one_kernel(pool_k):
+    """Convolutions followed by max-pools whose windows do not overlap run as
+    one kernel each (a lane group per pooled pixel): NaN inputs pass identity
+    convolutions and pools to the outputs (a ReLU on the last pool, for two
+    of the window shapes, clears them), conv outputs past the last whole
+    window are dropped as the pool drops them, and the second convolution
+    has 9 channels (a partial channel group)."""
+    g = np.random.default_rng(300 + 10 * pool_k[0] + pool_k[1])
+    S, H, W, C = 3, 23, 29, 2
+    imgs = [g.standard_normal((S, H, W)).astype(np.float32) for _ in range(C)]
+    imgs[0][1, 5, 7] = np.nan
+    imgs[1][2, 20, 3] = np.nan
+    layers = [wl.conv_layer(21, 0, C, 4, (3, 3), mode="zeros", act=0), {"kind": "pool", "kernel": pool_k},
+              wl.conv_layer(22, 0, 4, 9, (2, 2), padding="valid", act=0),
+              {"kind": "pool", "kernel": (2, 2), "act": int(pool_k in ((3, 3), (1, 3)))}]
+    model = {"kind": "cnn", "in_channels": C, "image": (H, W), "layers": layers}
+    h2, w2, c2 = oracle.cnn_shapes(model)[-1]
+    spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+            "bnd": [0, 0, 0]}
+    out_spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, h2, w2), (1, 1, 1)),
+                "bnd": [0, 0, 0]}
+    w = wl.Workload("convpool", 0, "f32", [C, c2], spec, out_spec, imgs,
+                    [wl.sentinel_like((S, h2, w2)) for _ in range(c2)], model)
+    got, var = _run(w)
+    assert var == "cnn_layers_f32", var
+    exp = _expected(w)
+    g2 = np.stack([a.reshape(-1) for a in got], 1)
+    e2 = np.stack([a.reshape(-1) for a in exp], 1)
+    assert np.array_equal(np.isnan(g2), np.isnan(e2))
+    ok = ~np.isnan(e2)
+    assert_close(np.where(ok, g2, 0), np.where(ok, e2, 0), RTOL["f32"], "conv + pool %s" % (pool_k,))
+
+
+@pytest.mark.parametrize("case", ["fc_only", "long_tail", "reduce_only"])
+def test_fully_connected_tails(case):
+    """The fully connected layers closing a stack run with the scatter in one
+    kernel: a stack of fully connected layers only (256 wide, one image per
+    block), more small layers than that kernel takes (the layer-by-layer
+    kernels instead), and a single wide-K layer (split K, then only the
+    partial sums, bias and scatter).  37 images: a ragged last block."""
+    g = np.random.default_rng(["fc_only", "long_tail", "reduce_only"].index(case) + 500)
+    S, H, W, C = 37, 12, 14, 2
+    if case == "fc_only":
+        layers = [wl.linear_layer(31, 0, H * W * C, 200), wl.linear_layer(32, 0, 200, 256),
+                  wl.linear_layer(33, 0, 256, 3, act=0)]
+    elif case == "long_tail":
+        layers = [wl.conv_layer(34, 0, C, 3, (3, 3), padding="valid"), wl.linear_layer(35, 0, 10 * 12 * 3, 32)]
+        layers += [wl.linear_layer(36 + k, 0, 32, 32) for k in range(5)] + [wl.linear_layer(41, 0, 32, 2, act=0)]
+    else:
+        layers = [wl.conv_layer(42, 0, C, 4, (3, 3), mode="circular"), {"kind": "pool", "kernel": (2, 2)},
+                  wl.linear_layer(43, 0, 6 * 7 * 4, 17, act=0)]
+    model = {"kind": "cnn", "in_channels": C, "image": (H, W), "layers": layers}
+    c2 = oracle.cnn_shapes(model)[-1][2]
+    imgs = [g.standard_normal((S, H, W)).astype(np.float32) for _ in range(C)]
+    spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+            "bnd": [0, 0, 0]}
+    w = wl.Workload("tail", 0, "f32", [C, c2], spec, wl.pointwise_spec(S), imgs,
+                    [wl.sentinel_like((S,)) for _ in range(c2)], model)
+    got, var = _run(w)
+    assert var == "cnn_layers_f32", var
+    _compare(got, _expected(w), "fully connected tail, %s" % case, _rtol_for(model))
+
+
 def test_window_map_channels_and_strided_views():
     """Channels from a 3x3 periodic window map (36 channels: layer by layer)
     and from column views of one array of structures (fused)."""
