@@ -693,6 +693,8 @@ bool cnn_use_fused(const hpacml_model *model, const hpacml_map *in, const hpacml
 hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out, hipStream_t st) {
     const CnnPlan &c = model->cnnp;
     const int64_t S = in->plan.n_points / ((int64_t)c.height * c.width);
+    if (S == 0)
+        return HPACML_OK;   // no images: nothing to read or write
     if (cnn_use_fused(model, in, out))
         return hip_status(launch_cnn_fused(in->m32, out->m32, in->tab_dev, out->tab_dev, model->fused, (int32_t)S,
                                            c.height, c.width, st));

@@ -854,7 +854,7 @@ void cnn_conv_pack(const float *W, int cout, int cin, int kh, int kw, std::vecto
 int linear_tile(const CnnLayerDev &L) { return L.cout > 16 ? 64 : 16; }
 
 int linear_splits(const CnnLayerDev &L, int64_t S) {
-    if (L.kind != HPACML_LAYER_LINEAR)
+    if (L.kind != HPACML_LAYER_LINEAR || S <= 0)
         return 1;
     const int64_t K = (int64_t)L.h * L.w * L.cin;
     const int64_t T = linear_tile(L);

@@ -241,6 +241,32 @@ def test_fully_connected_tails(case):
     _compare(got, _expected(w), "fully connected tail, %s" % case, _rtol_for(model))
 
 
+def test_zero_images_launch_nothing():
+    """Sweeps with no images: inference returns OK, writes nothing, and the
+    record of the (empty) input map is empty."""
+    import torch
+    H, W = 16, 16
+    model = {"kind": "cnn", "in_channels": 1, "image": (H, W),
+             "layers": [wl.conv_layer(51, 0, 1, 4, (4, 4), padding="valid", stride=(4, 4)),
+                        {"kind": "pool", "kernel": (2, 2)}, wl.linear_layer(52, 0, 2 * 2 * 4, 3, act=0)]}
+    frames = to_dev([np.ones((2, H, W), np.float32)])
+    spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((1, 0, 0), (1, H, W), (1, 1, 1)),
+            "bnd": [0, 0, 0]}
+    outs = to_dev([wl.sentinel_like((2,)) for _ in range(3)])
+    mi = api.Map(spec, frames, _abi.TO)
+    mo = api.Map({"rank": 1, "slices": [((0,), (1,))], "sweep": ((2,), (2,), (1,)), "bnd": [0]}, outs, _abi.FROM)
+    assert mi.n_points == 0 and mo.n_points == 0
+    m = api.CnnModel(model)
+    api.infer(m, mi, mo)
+    conv = api.CnnModel({"kind": "cnn", "in_channels": 1, "image": (H, W),
+                         "layers": [wl.conv_layer(53, 0, 1, 2, (3, 3), mode="circular")]})
+    mo2 = api.Map(spec, to_dev([wl.sentinel_like((2, H, W)) for _ in range(2)]), _abi.FROM)
+    api.infer(conv, mi, mo2)
+    torch.cuda.synchronize()
+    for o in outs:
+        assert np.array_equal(o.cpu().numpy().view(np.uint32), wl.sentinel_like((2,)).view(np.uint32))
+
+
 def test_window_map_channels_and_strided_views():
     """Channels from a 3x3 periodic window map (36 channels: layer by layer)
     and from column views of one array of structures (fused)."""
