@@ -87,16 +87,6 @@ template <int NMB, int KS1MAX, bool PF>
 __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout,
                                                       F32Packed pk, int32_t n_tiles) {
     extern __shared__ float lds[];
-    // stage the packed weights once per block
-    {
-        const float4 *src = reinterpret_cast<const float4 *>(pk.image);
-        float4 *dstl = reinterpret_cast<float4 *>(lds);
-        const int n4 = pk.lds_bytes / 16;
-        for (int i = threadIdx.x; i < n4; i += blockDim.x)
-            dstl[i] = src[i];
-    }
-    __syncthreads();
-
     const F32Layout lay{NMB, pk.ks1, pk.n_hidden, pk.f_out};
     const int lane = threadIdx.x & 63;
     const int g = lane >> 5;
@@ -139,13 +129,34 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatT
     // has no registers for a second set -- each tile is gathered just before
     // its use)
     constexpr bool kPrefetch = PF && !(NMB == 4 && KS1MAX == 32);
-    if (kPrefetch && wave_id < n_tiles)
+    // the first tile's loads go out before the weights are staged (their
+    // latencies overlap) where registers allow -- H = 64, or at most 16
+    // inputs (wider H = 128 variants would spill) -- and, without prefetch,
+    // when it is the wave's only tile
+    constexpr bool kEarly = NMB == 2 || KS1MAX <= 8;
+    bool gathered = false;
+    if (kEarly && wave_id < n_tiles && (kPrefetch || wave_id + n_waves >= n_tiles)) {
+        gather(wave_id);
+        gathered = true;
+    }
+
+    // stage the packed weights once per block
+    {
+        const float4 *src = reinterpret_cast<const float4 *>(pk.image);
+        float4 *dstl = reinterpret_cast<float4 *>(lds);
+        const int n4 = pk.lds_bytes / 16;
+        for (int i = threadIdx.x; i < n4; i += blockDim.x)
+            dstl[i] = src[i];
+    }
+    __syncthreads();
+    if (kPrefetch && !gathered && wave_id < n_tiles)
         gather(wave_id);
 
     for (int tile = wave_id; tile < n_tiles; tile += n_waves) {
         const int b = tile * 32 + col;
-        if (!kPrefetch)
+        if (!kPrefetch && !gathered)
             gather(tile);
+        gathered = false;
         const bool valid = nvalid;
         float x[KS1MAX];
 #pragma unroll
