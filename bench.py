@@ -95,6 +95,10 @@ def main():
     ap.add_argument("--inplace", action="store_true",
                     help="write the outputs back into the input fields (a time step advanced in place: windowed "
                          "maps then run the snapshot pass); no oracle leg, the fields change every step")
+    ap.add_argument("--phases", action="store_true",
+                    help="also time the model on the composed input tensor stored as dense column arrays (a "
+                         "gather with nothing to compose): the fused kernel's time minus that is the cost of "
+                         "mapping (reported under phases; MLP workloads)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU work for the oracle sample")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="before warm-up, run one device-to-device copy of this many MiB (a kernel of "
@@ -285,6 +289,51 @@ def main():
                                   "points_per_s": B / (per_call * 1e-3),
                                   "achieved_tflops": flop_launch / (per_call * 1e-3) / 1e12,
                                   "frac": flop_launch / (per_call * 1e-3) / peak}
+
+    if args.phases and not is_cnn:
+        # mapping vs inference: the composed tensor (the input record) as F
+        # contiguous column arrays under a pointwise map, outputs to Fo fresh
+        # arrays, through the same fused kernel family
+        api.collect(mi, rec_in, Fi, stream)
+        torch.cuda.synchronize()
+        cols = [rec_in[:, f].contiguous() for f in range(Fi)]
+        dense_out = [torch.empty(B, device="cuda") for _ in range(Fo)]
+        pw = {"rank": 1, "slices": [((0,), (1,))], "sweep": ((0,), (B,), (1,)), "bnd": [0]}
+        mci = api.Map(pw, cols, _abi.TO)
+        mco = api.Map(pw, dense_out, _abi.FROM)
+        reps = max(3, min(args.steps, 20))
+
+        def timed(fn):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps
+
+        # the three in turn over 5 rounds (medians), so that clock changes
+        # during the run fall on all of them
+        runs = {"dense": [], "fused": [], "gather": []}
+        for rnd in range(6):
+            d = timed(lambda: api.infer(model, mci, mco, stream))
+            f = timed(lambda: api.infer(model, mi, mo, stream))
+            c = timed(lambda: api.collect(mi, rec_in, Fi, stream))
+            if rnd:
+                runs["dense"].append(d)
+                runs["fused"].append(f)
+                runs["gather"].append(c)
+        dense_ms, fused_ms, gather_ms = (float(np.median(runs[k])) for k in ("dense", "fused", "gather"))
+        result["phases"] = {
+            "fused_ms": fused_ms, "dense_columns_ms": dense_ms, "dense_columns_kernel": api.variant(model, mci, mco),
+            "mapping_ms": fused_ms - dense_ms, "mapping_frac": (fused_ms - dense_ms) / fused_ms,
+            "gather_alone_ms": gather_ms,
+            "note": "back-to-back launches, medians of 5 interleaved rounds; mapping_ms = the fused region's "
+                    "time minus the same model on the composed tensor stored as dense columns; "
+                    "gather_alone_ms = the input map's collect"}
+        del cols, dense_out
+        mci.close()
+        mco.close()
 
     if not args.no_cpu_baseline and is_cnn:
         import oracle
