@@ -20,8 +20,12 @@
 // computes the pixel at the clamped position (inside the region, since the
 // region always contains the image edge it crosses).
 //
-// Layer-by-layer path: one kernel per layer over [S][h][w][c] workspaces
-// (one thread per output element), then a scatter of the last tensor.
+// Layer-by-layer path (everything else, and in-place regions): kernels over
+// [S][h][w][c] tensors in a workspace -- convolutions (a max-pool with
+// non-overlapping windows folded into the convolution before it), pools,
+// fully connected layers (split K when the tiles alone are too few), and the
+// fully connected layers closing a stack together with the scatter; else a
+// scatter of the last tensor.
 #include "cnn.hpp"
 
 namespace hpacml {
