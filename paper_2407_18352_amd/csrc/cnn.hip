@@ -863,8 +863,8 @@ int linear_splits(const CnnLayerDev &L, int64_t S) {
     const int64_t K = (int64_t)L.h * L.w * L.cin;
     const int64_t T = linear_tile(L);
     const int64_t blocks = ((S + T - 1) / T) * ((L.cout + T - 1) / T);
-    int64_t z = (512 + blocks - 1) / blocks;                   // about 512 blocks in all
-    z = std::min<int64_t>(z, std::max<int64_t>(1, K / 128));  // at least 128 k per block
+    int64_t z = (1024 + blocks - 1) / blocks;                 // about 1024 blocks in all
+    z = std::min<int64_t>(z, std::max<int64_t>(1, K / 64));  // at least 64 k per block
     return (int)std::max<int64_t>(1, std::min<int64_t>(z, kLinSplit));
 }
 
