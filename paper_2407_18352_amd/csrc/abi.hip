@@ -909,7 +909,7 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
         s = snapshot_map(in, &sm);
         if (s == HPACML_OK) {
             if (snapshot_feature_major(in)) {
-                CollectJob32 j = collect32_job(in->plan, in->m32, in->tab, (uint32_t *)in->snap, 1);
+                CollectJob32 j = collect32_job(in->plan, in->m32, in->tab, in->tab_dev, (uint32_t *)in->snap, 1);
                 j.dense = 0;
                 j.fs = in->plan.n_points;
                 s = hip_status(launch_collect32(&j, 1, st));
@@ -937,7 +937,7 @@ hpacml_status hpacml_collect(const hpacml_map *m, float *dst, int64_t ld, void *
         return s;
     uint32_t *d = reinterpret_cast<uint32_t *>(dst);
     if (m->t32) {
-        const CollectJob32 j = collect32_job(m->plan, m->m32, m->tab, d, ld);
+        const CollectJob32 j = collect32_job(m->plan, m->m32, m->tab, m->tab_dev, d, ld);
         return hip_status(launch_collect32(&j, 1, (hipStream_t)stream));
     }
     return hip_status(launch_collect(m->dev, d, ld, (hipStream_t)stream));
@@ -964,9 +964,9 @@ hpacml_status hpacml_collect_pair(const hpacml_map *a, float *dst_a, int64_t ld_
         CollectJob32 j[2];
         int n = 0;
         if (a->plan.n_points > 0)
-            j[n++] = collect32_job(a->plan, a->m32, a->tab, da, ld_a);
+            j[n++] = collect32_job(a->plan, a->m32, a->tab, a->tab_dev, da, ld_a);
         if (b->plan.n_points > 0)
-            j[n++] = collect32_job(b->plan, b->m32, b->tab, db, ld_b);
+            j[n++] = collect32_job(b->plan, b->m32, b->tab, b->tab_dev, db, ld_b);
         return n == 0 ? HPACML_OK : hip_status(launch_collect32(j, n, st));
     }
     // maps outside the 32-bit form: two launches, same result

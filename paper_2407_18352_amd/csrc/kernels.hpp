@@ -42,6 +42,7 @@ void table32_make(const MapPlan &p, FeatTable32 *out);
 struct CollectJob32 {
     Map32 m;
     FeatTable32 tab;
+    const FeatTable32 *tabp;   // device copy of tab (read instead of tab by launches of few features)
     uint32_t *dst;
     int64_t ld;
     uint32_t magic;      // idx / F by multiply-shift (idx < 2^16)
@@ -51,7 +52,8 @@ struct CollectJob32 {
     int32_t ppl;         // points per lane: 8, 4, 2 or 1 (F = 1, 2, 3-4, more)
     int64_t fs;          // 0: dst[p * ld + f]; else feature-major dst[f * fs + p] (ld unused)
 };
-CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &tab, uint32_t *dst, int64_t ld);
+CollectJob32 collect32_job(const MapPlan &p, const Map32 &m, const FeatTable32 &tab, const FeatTable32 *tab_dev,
+                           uint32_t *dst, int64_t ld);
 // One launch for one or two jobs (n_jobs in {1, 2}).
 hipError_t launch_collect32(const CollectJob32 *jobs, int n_jobs, hipStream_t stream);
 
