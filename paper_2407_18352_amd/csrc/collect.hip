@@ -278,10 +278,13 @@ hipError_t launch_collect32(const CollectJob32 *jobs, int n_jobs, hipStream_t st
     // LDS tile: the larger of the two jobs' U x 64 x F words
     const int w0 = j0.ppl * j0.m.n_features, w1 = j1.n_tiles ? j1.ppl * j1.m.n_features : 0;
     const size_t lds = (size_t)kP * (w0 > w1 ? w0 : w1) * sizeof(uint32_t);
-    // the table through its device pointer for launches of few features and
-    // at most 2 x 2^17 tiles (measured: 6-10% faster for the 6- and 9-feature
-    // pointwise records; 5% slower on a 2-million-tile launch)
-    if (j0.m.n_features <= 16 && (j1.n_tiles == 0 || j1.m.n_features <= 16) && grid <= 2 * kFuseMaxTiles)
+    // the table through its device pointer when the widest map has 5-16
+    // features (one point per lane) and the launch at most 2 x 2^17 tiles
+    // (measured: 6-13% faster for the 6- and 9-feature pointwise records;
+    // slower for maps of 1-4 features, several points per lane, for the
+    // wide windows and on a 2-million-tile launch)
+    const int fw = j1.n_tiles && j1.m.n_features > j0.m.n_features ? j1.m.n_features : j0.m.n_features;
+    if (fw >= 5 && fw <= 16 && grid <= 2 * kFuseMaxTiles)
         hipLaunchKernelGGL(collect32_kernel<true>, dim3((unsigned)grid), dim3(kP), lds, stream, j0, j1);
     else
         hipLaunchKernelGGL(collect32_kernel<false>, dim3((unsigned)grid), dim3(kP), lds, stream, j0, j1);
