@@ -79,6 +79,15 @@ def recorded_traffic(variant, workload):
     return None
 
 
+def cnn_hbm_bound(w, wl) -> bool:
+    """A convolutional workload is bound by HBM when moving its arrays once at
+    the HBM peak takes longer than its flops at the fp32 vector peak."""
+    H, W = w.model["image"]
+    n_img = w.n_points // (H * W)
+    fields_b = sum(a.nbytes for a in w.inputs) + sum(a.nbytes for a in w.outputs)
+    return fields_b / HBM_PEAK > wl.cnn_flops_per_image(w.model) * n_img / VALU_F32_PEAK
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -136,11 +145,7 @@ def main():
     # time at the fp32 vector peak than its arrays take at the HBM peak is
     # bound by HBM, and then every step reads a fresh copy of the batch
     # (rotation) so that the Infinity Cache does not serve it
-    hbm_bound = False
-    if is_cnn:
-        H, W = w.model["image"]
-        n_img = w.n_points // (H * W)
-        hbm_bound = fields_b / HBM_PEAK > wl.cnn_flops_per_image(w.model) * n_img / VALU_F32_PEAK
+    hbm_bound = is_cnn and cnn_hbm_bound(w, wl)
     rotate = args.rotate or hbm_bound
     model = api.CnnModel(w.model) if is_cnn else api.Model(w.model)
     sets = []
