@@ -232,9 +232,11 @@ hpacml_status hpacml_cnn_validate(int32_t in_channels, int32_t height, int32_t w
  * model either runs one fused kernel (convolution-only stacks of SAME, stride-1
  * layers of at most 16 channels whose padding modes are all CIRCULAR or none
  * CIRCULAR, on maps in the 32-bit form whose `from` targets do not meet the
- * `to` targets), or a layer-by-layer path through a workspace of
- * S * (largest layer tensor) * 3 floats that the model owns (allocated on first
- * need, grown as needed, freed with the model).  That path reads every input
+ * `to` targets), or a layer-by-layer path through a workspace that the model
+ * owns (allocated on first need, grown as needed, freed with the model): two
+ * tensors of S * (largest layer tensor) floats, plus the partial sums of fully
+ * connected layers whose K is split over blocks (at most 32 * S * outputs
+ * floats).  That path reads every input
  * before writing any output, so `from` targets may overlap `to` targets; calls
  * that share a model must not overlap in time on different streams.  Errors
  * as hpacml_cnn_validate, plus HPACML_E_NOMEM / HPACML_E_DEVICE. */
