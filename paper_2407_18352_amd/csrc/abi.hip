@@ -703,7 +703,7 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
     // gathered copy in the workspace); the outputs are scattered after the
     // last layer, so they may overwrite inputs
     hpacml_model *mm = const_cast<hpacml_model *>(model);
-    const int64_t per = S * c.max_elems;
+    const int64_t per = (S * c.max_elems + 63) / 64 * 64;   // 256-byte aligned buffers
     // split-K partial sums of the fully connected layers
     int64_t part_floats = 0;
     for (const CnnLayerDev &L : model->cnn_layers) {

@@ -32,6 +32,8 @@ namespace hpacml {
 
 namespace {
 
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
 constexpr int kThreads = 256;
 constexpr int kTX = 64;   // tile columns
 constexpr int kPix = 1;   // pixels per thread per pass
@@ -633,6 +635,96 @@ __global__ void __launch_bounds__(256) cnn_linear_kernel(CnnLayerDev L, const fl
     }
 }
 
+// The products of a fully connected layer with more than 16 outputs whose K
+// is split over blocks, on fp32 MFMA (v_mfma_f32_32x32x2f32): the transposed
+// product C[o][s] = sum_k W[o][k] in[s][k], weights as the A operand (32
+// outputs x 2 k per m-block), images as B (32 images x 2 k).  A block of 4
+// waves owns 128 images (32 per wave) x 64 outputs (2 m-blocks) and one K
+// range; K goes in chunks of kMfK staged in LDS (rows padded to kMfK + 1
+// floats: lane l reads row l % 32 at column k + l / 32, conflict-free),
+// loaded one chunk ahead in registers.  Lane l ends up holding image l % 32
+// and, in register r of m-block mb, output 32 mb + 8 (r / 4) + 4 (l / 32) +
+// r % 4: four consecutive outputs per group of registers, stored as one
+// 16-byte write of the raw partial sums part[z][s][o].
+constexpr int kMfS = 128, kMfO = 64, kMfK = 32;
+
+__global__ void __launch_bounds__(256) cnn_linear_mfma_kernel(CnnLayerDev L, const float *__restrict__ in, int64_t S,
+                                                             int64_t Kc, float *__restrict__ part) {
+    __shared__ float xs[kMfS][kMfK + 1];
+    __shared__ float ws[kMfO][kMfK + 1];
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    const int64_t s0 = (int64_t)blockIdx.x * kMfS;
+    const int o0 = blockIdx.y * kMfO;
+    const int O = L.cout;
+    const int64_t K = (int64_t)L.h * L.w * L.cin;
+    const int64_t kb = (int64_t)blockIdx.z * Kc;
+    const int64_t ke = kb + Kc < K ? kb + Kc : K;
+    // chunk loads: thread t takes column t % 32 of rows t / 32 + 8 m
+    const int c = t % kMfK, r0 = t / kMfK;
+    float xr[kMfS / 8], wr[kMfO / 8];
+    auto fetch = [&](int64_t k0) {
+        const int64_t k = k0 + c;
+        const bool kin = k < ke;
+#pragma unroll
+        for (int m = 0; m < kMfS / 8; ++m) {
+            const int64_t sr = s0 + r0 + 8 * m;
+            xr[m] = (kin && sr < S) ? in[sr * K + k] : 0.f;
+        }
+#pragma unroll
+        for (int m = 0; m < kMfO / 8; ++m) {
+            const int o = o0 + r0 + 8 * m;
+            wr[m] = (kin && o < O) ? L.W[(int64_t)o * K + k] : 0.f;
+        }
+    };
+    floatx16 acc[2];
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            acc[mb][r] = 0.f;
+    if (kb < ke)
+        fetch(kb);
+    const int col = lane & 31, kh = lane >> 5;
+    for (int64_t k0 = kb; k0 < ke; k0 += kMfK) {
+#pragma unroll
+        for (int m = 0; m < kMfS / 8; ++m)
+            xs[r0 + 8 * m][c] = xr[m];
+#pragma unroll
+        for (int m = 0; m < kMfO / 8; ++m)
+            ws[r0 + 8 * m][c] = wr[m];
+        __syncthreads();
+        if (k0 + kMfK < ke)
+            fetch(k0 + kMfK);
+#pragma unroll
+        for (int kk = 0; kk < kMfK; kk += 2) {
+            const float b = xs[32 * w + col][kk + kh];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+                acc[mb] = __builtin_amdgcn_mfma_f32_32x32x2f32(ws[32 * mb + col][kk + kh], b, acc[mb], 0, 0, 0);
+        }
+        __syncthreads();
+    }
+    const int64_t s = s0 + 32 * w + col;
+    if (s >= S)
+        return;
+    float *dst = part + ((int64_t)blockIdx.z * S + s) * O;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int o = o0 + 32 * mb + 8 * q + 4 * kh;
+            if (o + 3 < O && ((uintptr_t)(dst + o) & 15) == 0) {
+                *reinterpret_cast<float4 *>(dst + o) =
+                    make_float4(acc[mb][4 * q], acc[mb][4 * q + 1], acc[mb][4 * q + 2], acc[mb][4 * q + 3]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (o + i < O)
+                        dst[o + i] = acc[mb][4 * q + i];
+            }
+        }
+}
+
 __global__ void __launch_bounds__(256) cnn_linear_reduce_kernel(CnnLayerDev L, const float *__restrict__ part,
                                                                float *__restrict__ out, int64_t S, int splits) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -862,7 +954,10 @@ int linear_splits(const CnnLayerDev &L, int64_t S) {
         return 1;
     const int64_t K = (int64_t)L.h * L.w * L.cin;
     const int64_t T = linear_tile(L);
-    const int64_t blocks = ((S + T - 1) / T) * ((L.cout + T - 1) / T);
+    // split products of layers with more than 16 outputs run on the MFMA
+    // kernel's 128 x 64 tiles
+    const int64_t blocks = T == 64 ? ((S + kMfS - 1) / kMfS) * ((L.cout + kMfO - 1) / kMfO)
+                                   : ((S + T - 1) / T) * ((L.cout + T - 1) / T);
     int64_t z = (1024 + blocks - 1) / blocks;                 // about 1024 blocks in all
     z = std::min<int64_t>(z, std::max<int64_t>(1, K / 64));  // at least 64 k per block
     return (int)std::max<int64_t>(1, std::min<int64_t>(z, kLinSplit));
@@ -895,6 +990,28 @@ hipError_t launch_cnn_conv(const CnnLayerDev &L, const CnnLayerDev *pool, const 
     return hipGetLastError();
 }
 
+// Raw split-K partial sums of a fully connected layer into part[splits][S][O]
+// (splits >= 2).
+hipError_t launch_linear_split(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part, int splits,
+                               hipStream_t stream) {
+    const int64_t K = (int64_t)L.h * L.w * L.cin;
+    const int64_t Kc = (K + splits - 1) / splits;
+    if (linear_tile(L) == 64) {
+        const int64_t bx = (S + kMfS - 1) / kMfS, by = (L.cout + kMfO - 1) / kMfO;
+        if (bx > INT32_MAX || by > 65535)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL(cnn_linear_mfma_kernel, dim3((unsigned)bx, (unsigned)by, splits), dim3(256), 0, stream, L,
+                           in, S, Kc, part);
+    } else {
+        const int64_t bx = (S + 15) / 16, by = (L.cout + 15) / 16;
+        if (bx > INT32_MAX || by > 65535)
+            return hipErrorInvalidValue;
+        hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by, splits), dim3(256), 0, stream, L,
+                           in, out, S, Kc, part);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, int64_t S, float *part,
                             hipStream_t stream) {
     const int64_t total = S * (int64_t)L.h2 * L.w2 * L.cout;
@@ -913,21 +1030,20 @@ hipError_t launch_cnn_layer(const CnnLayerDev &L, const float *in, float *out, i
         // K split over up to kLinSplit blocks when the tiles alone leave the
         // chip short of blocks
         const int T = linear_tile(L);
-        const bool big = T == 64;
-        const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
-        if (bx > INT32_MAX || by > 65535)
-            return hipErrorInvalidValue;
-        const int64_t K = (int64_t)L.h * L.w * L.cin;
         const int splits = linear_splits(L, S);
-        const int64_t Kc = (K + splits - 1) / splits;
-        if (big)
-            hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by, splits), dim3(256), 0, stream,
-                               L, in, out, S, Kc, part);
-        else
-            hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by, splits), dim3(256), 0, stream,
-                               L, in, out, S, Kc, part);
-        if (splits > 1) {
-            hipError_t e = hipGetLastError();
+        if (splits == 1) {
+            const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
+            if (bx > INT32_MAX || by > 65535)
+                return hipErrorInvalidValue;
+            const int64_t K = (int64_t)L.h * L.w * L.cin;
+            if (T == 64)
+                hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by, 1), dim3(256), 0, stream,
+                                   L, in, out, S, K, part);
+            else
+                hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by, 1), dim3(256), 0, stream,
+                                   L, in, out, S, K, part);
+        } else {
+            hipError_t e = launch_linear_split(L, in, out, S, part, splits, stream);
             if (e != hipSuccess)
                 return e;
             const int64_t n = S * L.cout;
@@ -984,19 +1100,7 @@ hipError_t launch_cnn_linear_partials(const CnnLayerDev &L, const float *in, flo
     *splits = linear_splits(L, S);
     if (*splits <= 1)
         return launch_cnn_layer(L, in, out, S, part, stream);
-    const int T = linear_tile(L);
-    const int64_t bx = (S + T - 1) / T, by = (L.cout + T - 1) / T;
-    if (bx > INT32_MAX || by > 65535)
-        return hipErrorInvalidValue;
-    const int64_t K = (int64_t)L.h * L.w * L.cin;
-    const int64_t Kc = (K + *splits - 1) / *splits;
-    if (T == 64)
-        hipLaunchKernelGGL(cnn_linear_kernel<64>, dim3((unsigned)bx, (unsigned)by, *splits), dim3(256), 0, stream, L,
-                           in, out, S, Kc, part);
-    else
-        hipLaunchKernelGGL(cnn_linear_kernel<16>, dim3((unsigned)bx, (unsigned)by, *splits), dim3(256), 0, stream, L,
-                           in, out, S, Kc, part);
-    return hipGetLastError();
+    return launch_linear_split(L, in, out, S, part, *splits, stream);
 }
 
 hipError_t launch_scatter_record(const DevMap &m, const float *src, hipStream_t stream) {
