@@ -759,10 +759,16 @@ __global__ void __launch_bounds__(256) cnn_tail_kernel(CnnTail T, const float *_
             float v;
             if (T.splits) {
                 const int64_t n = S * L.cout, idx = s * L.cout + o;
+                // every partial in flight before the first add; the sum in block order
+                float pv[kLinSplit];
+#pragma unroll
+                for (int z = 0; z < kLinSplit; ++z)
+                    pv[z] = z < T.splits ? src[z * n + idx] : 0.f;
                 v = 0.f;
-#pragma unroll 8
-                for (int z = 0; z < T.splits; ++z)
-                    v += src[z * n + idx];
+#pragma unroll
+                for (int z = 0; z < kLinSplit; ++z)
+                    if (z < T.splits)
+                        v += pv[z];
                 v += L.b[o];
                 v = L.act == HPACML_ACT_RELU ? (v > 0.f ? v : 0.f) : v;
             } else {
