@@ -658,6 +658,7 @@ hpacml_status hpacml_cnn_create(int32_t in_channels, int32_t height, int32_t wid
             d.w2 = p.shape[l + 1].w;
             d.W = m->cnn_buf + woff[l];
             d.b = m->cnn_buf + boff[l];
+            cnn_layer_divisors(d);
             m->cnn_layers.push_back(d);
         }
         m->cnnp = std::move(p);

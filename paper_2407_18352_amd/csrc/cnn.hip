@@ -474,6 +474,10 @@ __device__ __forceinline__ void conv_pixel(const CnnLayerDev &L, const float *im
         acc[g] = L.act == HPACML_ACT_RELU ? (acc[g] > 0.f ? acc[g] : 0.f) : acc[g];
 }
 
+__device__ __forceinline__ uint32_t fdiv(uint32_t i, uint32_t magic, uint32_t shift) {
+    return (uint32_t)(((uint64_t)i * magic) >> shift);
+}
+
 template <bool POOL>
 __global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, CnnLayerDev P, int qshift,
                                                       const float *__restrict__ in, float *__restrict__ out,
@@ -486,15 +490,31 @@ __global__ void __launch_bounds__(256) cnn_conv_kernel(CnnLayerDev L, CnnLayerDe
     const int64_t pc = pix < n_pix ? pix : n_pix - 1;
     const int co0 = blockIdx.y * kConvG;
     const int ng = min(kConvG, L.cout - co0);
-    const int W2 = POOL ? P.w2 : L.w2, H2 = POOL ? P.h2 : L.h2;
-    int ox = (int)(pc % W2);
-    int oy = (int)(pc / W2 % H2);
-    const int64_t s = pc / ((int64_t)W2 * H2);
+    const CnnLayerDev &G = POOL ? P : L;   // the grid of output pixels
+    int ox, oy;
+    int64_t s;
+    if (n_pix <= INT32_MAX) {
+        // 32-bit divisions by multiply-shift (a 64-bit division is a long
+        // instruction sequence, and this kernel is VALU-bound)
+        const uint32_t q1 = fdiv((uint32_t)pc, G.w2_magic, G.w2_shift);
+        const uint32_t q2 = fdiv(q1, G.h2_magic, G.h2_shift);
+        ox = (int)((uint32_t)pc - q1 * (uint32_t)G.w2);
+        oy = (int)(q1 - q2 * (uint32_t)G.h2);
+        s = q2;
+    } else {
+        ox = (int)(pc % G.w2);
+        oy = (int)(pc / G.w2 % G.h2);
+        s = pc / ((int64_t)G.w2 * G.h2);
+    }
     const int q = POOL ? (int)(tid & ((1 << qshift) - 1)) : 0;
     if (POOL) {
+        // window position qq < 16 of a window kw <= 16 wide: (qq + 1/2) / kw
+        // lies at least 1/32 from an integer, so the approximate reciprocal
+        // gives the exact quotient
         const int qq = q < P.kh * P.kw ? q : 0;
-        oy = oy * P.sh + qq / P.kw;
-        ox = ox * P.sw + qq % P.kw;
+        const int qy = (int)(((float)qq + 0.5f) * __builtin_amdgcn_rcpf((float)P.kw));
+        oy = oy * P.sh + qy;
+        ox = ox * P.sw + (qq - qy * P.kw);
     }
     const float *img = in + s * L.h * L.w * L.cin;
     const float *__restrict__ wg = L.W + (int64_t)blockIdx.y * L.kh * L.kw * L.cin * kConvG;
@@ -936,6 +956,20 @@ hipError_t launch_cnn_fused(const Map32 &in, const Map32 &out, const FeatTable32
         return e;
     hipLaunchKernelGGL(cnn_fused_kernel, dim3((unsigned)n_tiles), dim3(kThreads), lds, stream, a, f.wts);
     return hipGetLastError();
+}
+
+static void divisor(uint32_t d, uint32_t *magic, uint32_t *shift) {
+    // i / d == (i * magic) >> (31 + l) for i < 2^31, l = ceil(log2 d), d < 2^31
+    int l = 0;
+    while ((uint64_t(1) << l) < d)
+        ++l;
+    *magic = (uint32_t)(((uint64_t(1) << (31 + l)) + d - 1) / d);
+    *shift = 31 + l;
+}
+
+void cnn_layer_divisors(CnnLayerDev &L) {
+    divisor((uint32_t)std::max(L.w2, 1), &L.w2_magic, &L.w2_shift);
+    divisor((uint32_t)std::max(L.h2, 1), &L.h2_magic, &L.h2_shift);
 }
 
 void cnn_conv_pack(const float *W, int cout, int cin, int kh, int kw, std::vector<float> &dst) {

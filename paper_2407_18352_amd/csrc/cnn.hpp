@@ -15,9 +15,13 @@ constexpr int kConvG = 8;           // output channels per convolution thread
 struct CnnLayerDev {
     int32_t kind, cin, cout, kh, kw, sh, sw, same, mode, act;
     int32_t h, w, h2, w2;          // input and output image sizes
+    // i / w2 == (i * w2_magic) >> w2_shift for i < 2^31 (and likewise h2)
+    uint32_t w2_magic, w2_shift, h2_magic, h2_shift;
     const float *W, *b;            // device: convolution weights packed by
                                    // cnn_conv_pack, else the caller's layouts
 };
+// Sets the division constants of L.w2 and L.h2.
+void cnn_layer_divisors(CnnLayerDev &L);
 // Convolution weights [cout][cin][kh][kw] -> [ceil(cout / kConvG)][kh][kw][cin]
 // [kConvG], zero past cout (appended to `dst`).
 void cnn_conv_pack(const float *W, int cout, int cin, int kh, int kw, std::vector<float> &dst);
