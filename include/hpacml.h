@@ -231,8 +231,10 @@ hpacml_status hpacml_cnn_validate(int32_t in_channels, int32_t height, int32_t w
  * Weights are copied to library-owned device memory.  hpacml_infer with such a
  * model either runs one fused kernel (convolution-only stacks of SAME, stride-1
  * layers of at most 16 channels whose padding modes are all CIRCULAR or none
- * CIRCULAR, on maps in the 32-bit form whose `from` targets do not meet the
- * `to` targets), or a layer-by-layer path through a workspace that the model
+ * CIRCULAR, on maps in the 32-bit form; when the `from` targets meet the `to`
+ * targets, the inputs are first copied into the `to` map's snapshot record
+ * and the kernel reads them there), or a layer-by-layer path through a
+ * workspace that the model
  * owns (allocated on first need, grown as needed, freed with the model): two
  * tensors of S * (largest layer tensor) floats, plus the partial sums of fully
  * connected layers whose K is split over blocks (at most 32 * S * outputs

@@ -683,11 +683,23 @@ bool maps_disjoint(const MapPlan &a, const MapPlan &b) {
     return true;
 }
 
+// (defined with the snapshot record below)
+bool snapshot_t32(const hpacml_map *in);
+hpacml_status take_snapshot(const hpacml_map *in, hipStream_t st, const hpacml_map **sm);
+
 // The fused convolution kernel takes this call: 32-bit maps, outputs that
 // meet no input (its tiles read their neighbours' pixels), and a tile that
 // fits in LDS.
 bool cnn_use_fused(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
     return model->cnn_fused && in->t32 && out->t32 && maps_disjoint(in->plan, out->plan) &&
+           cnn_fused_tile_rows(model->fused, model->cnnp.height) > 0;
+}
+
+// Outputs that meet the inputs (a step written back into its own fields):
+// the fused kernel still runs when it reads the inputs from the `to` map's
+// snapshot record, filled first.
+bool cnn_fused_on_snapshot(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
+    return model->cnn_fused && in->t32 && out->t32 && !maps_disjoint(in->plan, out->plan) && snapshot_t32(in) &&
            cnn_fused_tile_rows(model->fused, model->cnnp.height) > 0;
 }
 
@@ -699,6 +711,14 @@ hpacml_status cnn_infer(const hpacml_model *model, const hpacml_map *in, const h
     if (cnn_use_fused(model, in, out))
         return hip_status(launch_cnn_fused(in->m32, out->m32, in->tab_dev, out->tab_dev, model->fused, (int32_t)S,
                                            c.height, c.width, st));
+    if (cnn_fused_on_snapshot(model, in, out)) {
+        const hpacml_map *sm = nullptr;
+        hpacml_status s = take_snapshot(in, st, &sm);
+        if (s != HPACML_OK)
+            return s;
+        return hip_status(launch_cnn_fused(sm->m32, out->m32, sm->tab_dev, out->tab_dev, model->fused, (int32_t)S,
+                                           c.height, c.width, st));
+    }
     // layer by layer: the first layer reads the map's tensor (the input
     // array itself when the map is a plain row-major view of it, else a
     // gathered copy in the workspace); the outputs are scattered after the
@@ -870,6 +890,21 @@ const char *kernel_name(const hpacml_model *model, bool fast) {
     }
 }
 
+// Every input of `in` into its snapshot record (stream-ordered before what
+// follows); *sm = the map that reads the record.
+hpacml_status take_snapshot(const hpacml_map *in, hipStream_t st, const hpacml_map **sm) {
+    hpacml_status s = snapshot_map(in, sm);
+    if (s != HPACML_OK)
+        return s;
+    if (snapshot_feature_major(in)) {
+        CollectJob32 j = collect32_job(in->plan, in->m32, in->tab, in->tab_dev, (uint32_t *)in->snap, 1);
+        j.dense = 0;
+        j.fs = in->plan.n_points;
+        return hip_status(launch_collect32(&j, 1, st));
+    }
+    return hpacml_collect(in, in->snap, in->plan.n_features, st);
+}
+
 // "snapshot+" prefixed names, kept for the life of the process
 const char *snapshot_name(const char *kernel) {
     static std::mutex mu;
@@ -885,7 +920,9 @@ const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in
     if (check_infer(model, in, out, &snapshot) != HPACML_OK)
         return nullptr;
     if (model->cnn)
-        return cnn_use_fused(model, in, out) ? "cnn_fused_f32" : "cnn_layers_f32";
+        return cnn_use_fused(model, in, out)           ? "cnn_fused_f32"
+               : cnn_fused_on_snapshot(model, in, out) ? "snapshot+cnn_fused_f32"
+                                                       : "cnn_layers_f32";
     if (!snapshot)
         return kernel_name(model, in->t32 && out->t32);
     return snapshot_name(kernel_name(model, snapshot_t32(in) && out->t32));
@@ -907,17 +944,7 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
         // every point's inputs go to the snapshot record first, and the model
         // then reads them from there (stream order separates the two passes)
         const hpacml_map *sm = nullptr;
-        s = snapshot_map(in, &sm);
-        if (s == HPACML_OK) {
-            if (snapshot_feature_major(in)) {
-                CollectJob32 j = collect32_job(in->plan, in->m32, in->tab, in->tab_dev, (uint32_t *)in->snap, 1);
-                j.dense = 0;
-                j.fs = in->plan.n_points;
-                s = hip_status(launch_collect32(&j, 1, st));
-            } else {
-                s = hpacml_collect(in, in->snap, in->plan.n_features, stream);
-            }
-        }
+        s = take_snapshot(in, st, &sm);
         if (s != HPACML_OK)
             return s;
         in = sm;

@@ -301,15 +301,35 @@ def test_window_map_channels_and_strided_views():
     _compare([o.cpu().numpy() for o in outs], exp, "array of structures")
 
 
-def test_inplace_update_reads_every_input_first():
-    """A MiniWeather-like step written back into its own fields: the fused
-    tiles would read pixels other tiles have overwritten, so the layer-by-
-    layer path (every input gathered first) runs, and matches the oracle's
-    region on the same arrays."""
+@pytest.mark.parametrize("stack", ["fused", "layers"])
+def test_inplace_update_reads_every_input_first(stack):
+    """A MiniWeather-like step written back into its own fields.  The fused
+    tiles would read pixels other tiles have overwritten, so the inputs go to
+    the map's snapshot record first and the fused kernel reads them there; a
+    stack the fused kernel does not take (circular and zero padding mixed)
+    runs layer by layer (every input gathered first).  Both match the
+    oracle's region on the same arrays, and a second step reuses the
+    snapshot record."""
+    import torch
     w = wl.make_cnn("weather_cnn", (29, 70))
-    got, var = _run(w, fields_out="inplace")
-    assert var == "cnn_layers_f32"
-    _compare(got, _expected(w, inplace=True), "in place")
+    want = "snapshot+cnn_fused_f32"
+    if stack == "layers":
+        model = {"kind": "cnn", "in_channels": 4, "image": (29, 70),
+                 "layers": [wl.conv_layer(61, 0, 4, 6, (3, 3), mode="circular"),
+                            wl.conv_layer(62, 0, 6, 4, (3, 3), mode="zeros", act=0)]}
+        w = wl.Workload("inplace_layers", 0, "f32", [4, 4], w.in_spec, w.out_spec, w.inputs, w.outputs, model)
+        want = "cnn_layers_f32"
+    fields = to_dev(w.inputs)
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.CnnModel(w.model)
+    assert api.variant(m, mi, mo) == want
+    exp = [a.copy() for a in w.inputs]
+    for step in range(2):
+        api.infer(m, mi, mo)
+        oracle.infer(w.in_spec, exp, w.out_spec, exp, w.model)
+        torch.cuda.synchronize()
+        _compare([f.cpu().numpy() for f in fields], exp, "in place (%s), step %d" % (stack, step))
 
 
 def test_pool_nan_propagates_and_relu_clears_nan():
