@@ -92,7 +92,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="bonds", choices=sorted(DESCRIPTION))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rotate", action="store_true",
