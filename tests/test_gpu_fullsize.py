@@ -86,6 +86,27 @@ def test_cnn_fullsize(name):
     print("%s full [%s]: worst scaled %.3e, normwise %.3e" % (name, var, worst, norm))
 
 
+def test_cnn_inplace_fullsize():
+    """The 2048 x 2048 convolutional step written back into its own four
+    fields: the inputs go to the snapshot record and the fused kernel reads
+    them there; every pixel against the oracle's region (all gathers, then
+    the model, then all writes) on the original fields."""
+    import torch
+    w = wl.make_cnn("weather_cnn")
+    fields = [torch.from_numpy(a).cuda() for a in w.inputs]
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.CnnModel(w.model)
+    var = api.variant(m, mi, mo)
+    assert var == "snapshot+cnn_fused_f32", var
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    got = np.stack([f.cpu().numpy().reshape(-1) for f in fields], 1)
+    Y = oracle.cnn(w.model, oracle.gather(w.in_spec, w.inputs))
+    worst, norm = assert_close(got, Y, RTOL["f32"], "weather_cnn full, in place via %s" % var)
+    print("weather_cnn full in place [%s]: worst scaled %.3e, normwise %.3e" % (var, worst, norm))
+
+
 @pytest.mark.parametrize("name", ["stencil2d", "stencil3d"])
 def test_inplace_step_fullsize_sampled(name):
     """One step written back into the fields it reads, at full size: the
