@@ -192,3 +192,46 @@ def test_collect_around_a_convolutional_region():
     oracle.infer(w.in_spec, w.inputs, w.out_spec, exp, w.model)
     got = np.stack([o.cpu().numpy() for o in outs], 1)
     assert_close(got, np.stack(exp, 1), RTOL["f32"], "convolutional inference through a region")
+
+
+def test_predicated_region_over_an_in_place_convolutional_step():
+    """A MiniWeather-like step that writes its own fields, as a predicated
+    region: inference invocations run the fused convolution on the snapshot
+    of the fields; collecting invocations record the fields before and after
+    the accurate path (here: every field scaled by 1/2)."""
+    import torch
+    w = wl.make_cnn("weather_cnn", (24, 70))
+    fields = to_dev(w.inputs)
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.CnnModel(w.model)
+    assert api.variant(m, mi, mo) == "snapshot+cnn_fused_f32"
+    r = api.Region(m, mi, mo, _abi.MODE_PREDICATED, capacity=2)
+
+    def accurate(handle):
+        st = torch.cuda.ExternalStream(handle) if handle else torch.cuda.default_stream()
+        with torch.cuda.stream(st):
+            for f in fields:
+                f.mul_(0.5)
+
+    exp = [a.copy() for a in w.inputs]
+    recs = []
+    for k, cond in enumerate([True, False, True, False]):
+        r.run(accurate, cond=cond)
+        if cond:
+            oracle.infer(w.in_spec, exp, w.out_spec, exp, w.model)
+        else:
+            recs.append(oracle.collect(w.in_spec, exp))
+            exp = [(a * np.float32(0.5)).astype(np.float32) for a in exp]
+            recs.append(oracle.collect(w.out_spec, exp))
+        torch.cuda.synchronize()
+        got = np.stack([f.cpu().numpy().reshape(-1) for f in fields], 1)
+        assert_close(got, np.stack([a.reshape(-1) for a in exp], 1), RTOL["f32"], "invocation %d" % k)
+        # carry the GPU's state forward so later comparisons see the same inputs
+        exp = [f.cpu().numpy().copy() for f in fields]
+    assert r.samples == 2
+    ins, outs, t = r.read()
+    for j in range(2):
+        assert np.array_equal(ins[j].view(np.uint32), recs[2 * j]), j
+        assert np.array_equal(outs[j].view(np.uint32), recs[2 * j + 1]), j
+    assert np.all(t > 0)
