@@ -125,6 +125,16 @@ class Model:
         L = len(dims) - 1
         self.W = [np.ascontiguousarray(np.asarray(w, dtype=np.float32)) for w in spec["W"]]
         self.b = [np.ascontiguousarray(np.asarray(b, dtype=np.float32)) for b in spec["b"]]
+        # the library reads dims[l+1] x dims[l] weights through a plain pointer:
+        # arrays of another size are refused here (invalid dims are left to
+        # the library's own status)
+        if len(self.W) != L or len(self.b) != L:
+            raise ValueError("model spec: %d weight and %d bias arrays for %d layers" % (len(self.W), len(self.b), L))
+        if min(dims) > 0:
+            for l in range(L):
+                if self.W[l].size != dims[l + 1] * dims[l] or self.b[l].size != dims[l + 1]:
+                    raise ValueError("layer %d: weights of %d and biases of %d values, expected %d x %d and %d"
+                                     % (l, self.W[l].size, self.b[l].size, dims[l + 1], dims[l], dims[l + 1]))
         Wp = (C.POINTER(C.c_float) * L)(*[w.ctypes.data_as(C.POINTER(C.c_float)) for w in self.W])
         bp = (C.POINTER(C.c_float) * L)(*[b.ctypes.data_as(C.POINTER(C.c_float)) for b in self.b])
         d = (C.c_int32 * (L + 1))(*dims)
@@ -194,6 +204,27 @@ class CnnModel:
                   for ly in Ls]
         self.b = [None if ly["kind"] == "pool" else np.ascontiguousarray(np.asarray(ly["b"], np.float32))
                   for ly in Ls]
+        # weight and bias sizes per layer, for a description the library
+        # accepts (its own status reports the others)
+        if validate_cnn(spec)[0] == _abi.OK:
+            h, w, c = int(spec["image"][0]), int(spec["image"][1]), int(spec["in_channels"])
+            for l, ly in enumerate(Ls):
+                if ly["kind"] == "pool":
+                    (kh, kw), (sh, sw) = ly["kernel"], ly.get("stride", ly["kernel"])
+                    h, w = (h - kh) // sh + 1, (w - kw) // sw + 1
+                    continue
+                if ly["kind"] == "conv":
+                    (kh, kw), (sh, sw) = ly["kernel"], ly.get("stride", (1, 1))
+                    nw = ly["out"] * c * kh * kw
+                    if ly.get("padding", "valid") == "valid":
+                        h, w = (h - kh) // sh + 1, (w - kw) // sw + 1
+                else:
+                    nw = ly["out"] * h * w * c
+                    h = w = 1
+                c = ly["out"]
+                if self.W[l].size != nw or self.b[l].size != c:
+                    raise ValueError("layer %d: weights of %d and biases of %d values, expected %d and %d"
+                                     % (l, self.W[l].size, self.b[l].size, nw, c))
         null = C.POINTER(C.c_float)()
         Wp = (C.POINTER(C.c_float) * L)(*[null if w is None else w.ctypes.data_as(C.POINTER(C.c_float))
                                           for w in self.W])
