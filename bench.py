@@ -293,7 +293,9 @@ def main():
         result["graph_replay"] = {"calls": args.graph_calls, "ms_per_call": per_call,
                                   "points_per_s": B / (per_call * 1e-3),
                                   "achieved_tflops": flop_launch / (per_call * 1e-3) / 1e12,
-                                  "frac": flop_launch / (per_call * 1e-3) / peak}
+                                  "frac": (alg_bytes if hbm_bound else flop_launch) / (per_call * 1e-3) / peak}
+        if hbm_bound:
+            result["graph_replay"]["achieved_gbs"] = alg_bytes / (per_call * 1e-3) / 1e9
 
     if args.phases and not is_cnn:
         # mapping vs inference: the composed tensor (the input record) as F
