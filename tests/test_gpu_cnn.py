@@ -241,6 +241,25 @@ def test_fully_connected_tails(case):
     _compare(got, _expected(w), "fully connected tail, %s" % case, _rtol_for(model))
 
 
+def test_many_small_images_take_the_unsplit_kernels():
+    """140,000 images of 3x3: the tiles alone cover the chip, so the fully
+    connected layer of 32 outputs runs unsplit on the 64 x 64 VALU tiles and
+    the closing layer in the tail kernel; every image against the oracle."""
+    g = np.random.default_rng(800)
+    S, H, W = 140000, 3, 3
+    layers = [wl.conv_layer(71, 0, 1, 4, (2, 2), padding="valid"), wl.linear_layer(72, 0, 2 * 2 * 4, 32),
+              wl.linear_layer(73, 0, 32, 3, act=0)]
+    model = {"kind": "cnn", "in_channels": 1, "image": (H, W), "layers": layers}
+    frames = g.standard_normal((S, H, W)).astype(np.float32)
+    spec = {"rank": 3, "slices": [((0, 0, 0), (1, 1, 1))], "sweep": ((0, 0, 0), (S, H, W), (1, 1, 1)),
+            "bnd": [0, 0, 0]}
+    w = wl.Workload("many", 0, "f32", [1, 3], spec, wl.pointwise_spec(S), [frames],
+                    [wl.sentinel_like((S,)) for _ in range(3)], model)
+    got, var = _run(w)
+    assert var == "cnn_layers_f32", var
+    _compare(got, _expected(w), "many small images")
+
+
 def test_zero_images_launch_nothing():
     """Sweeps with no images: inference returns OK, writes nothing, and the
     record of the (empty) input map is empty."""
