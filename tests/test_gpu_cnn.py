@@ -320,7 +320,7 @@ def test_window_map_channels_and_strided_views():
     _compare([o.cpu().numpy() for o in outs], exp, "array of structures")
 
 
-@pytest.mark.parametrize("stack", ["fused", "layers"])
+@pytest.mark.parametrize("stack", ["fused", "layers", "single_field"])
 def test_inplace_update_reads_every_input_first(stack):
     """A MiniWeather-like step written back into its own fields.  The fused
     tiles would read pixels other tiles have overwritten, so the inputs go to
@@ -338,6 +338,13 @@ def test_inplace_update_reads_every_input_first(stack):
                             wl.conv_layer(62, 0, 6, 4, (3, 3), mode="zeros", act=0)]}
         w = wl.Workload("inplace_layers", 0, "f32", [4, 4], w.in_spec, w.out_spec, w.inputs, w.outputs, model)
         want = "cnn_layers_f32"
+    elif stack == "single_field":
+        # one field: the snapshot record is row-major [points][1]
+        model = {"kind": "cnn", "in_channels": 1, "image": (29, 70),
+                 "layers": [wl.conv_layer(63, 0, 1, 4, (3, 3), mode="circular"),
+                            wl.conv_layer(64, 0, 4, 1, (3, 3), mode="circular", act=0)]}
+        w = wl.Workload("inplace_single", 0, "f32", [1, 1], w.in_spec, w.out_spec, w.inputs[:1], w.outputs[:1],
+                        model)
     fields = to_dev(w.inputs)
     mi = api.Map(w.in_spec, fields, _abi.TO)
     mo = api.Map(w.out_spec, fields, _abi.FROM)
