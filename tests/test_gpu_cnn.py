@@ -211,14 +211,18 @@ def test_conv_then_pool_in_one_kernel(pool_k):
     assert_close(np.where(ok, g2, 0), np.where(ok, e2, 0), RTOL["f32"], "conv + pool %s" % (pool_k,))
 
 
-@pytest.mark.parametrize("case", ["fc_only", "long_tail", "reduce_only"])
+TAIL_CASES = ["fc_only", "long_tail", "reduce_only", "two_closing"]
+
+
+@pytest.mark.parametrize("case", TAIL_CASES)
 def test_fully_connected_tails(case):
     """The fully connected layers closing a stack run with the scatter in one
     kernel: a stack of fully connected layers only (256 wide, one image per
     block), more small layers than that kernel takes (the layer-by-layer
-    kernels instead), and a single wide-K layer (split K, then only the
-    partial sums, bias and scatter).  37 images: a ragged last block."""
-    g = np.random.default_rng(["fc_only", "long_tail", "reduce_only"].index(case) + 500)
+    kernels instead), a single wide-K layer (split K, then only the partial
+    sums, bias and scatter), and a split-K layer followed by two small
+    layers of different widths.  37 images: a ragged last block."""
+    g = np.random.default_rng(TAIL_CASES.index(case) + 500)
     S, H, W, C = 37, 12, 14, 2
     if case == "fc_only":
         layers = [wl.linear_layer(31, 0, H * W * C, 200), wl.linear_layer(32, 0, 200, 256),
@@ -226,9 +230,12 @@ def test_fully_connected_tails(case):
     elif case == "long_tail":
         layers = [wl.conv_layer(34, 0, C, 3, (3, 3), padding="valid"), wl.linear_layer(35, 0, 10 * 12 * 3, 32)]
         layers += [wl.linear_layer(36 + k, 0, 32, 32) for k in range(5)] + [wl.linear_layer(41, 0, 32, 2, act=0)]
-    else:
+    elif case == "reduce_only":
         layers = [wl.conv_layer(42, 0, C, 4, (3, 3), mode="circular"), {"kind": "pool", "kernel": (2, 2)},
                   wl.linear_layer(43, 0, 6 * 7 * 4, 17, act=0)]
+    else:
+        layers = [wl.conv_layer(44, 0, C, 8, (3, 3), mode="zeros"), wl.linear_layer(45, 0, H * W * 8, 48),
+                  wl.linear_layer(46, 0, 48, 40), wl.linear_layer(47, 0, 40, 5, act=0)]
     model = {"kind": "cnn", "in_channels": C, "image": (H, W), "layers": layers}
     c2 = oracle.cnn_shapes(model)[-1][2]
     imgs = [g.standard_normal((S, H, W)).astype(np.float32) for _ in range(C)]
