@@ -629,14 +629,18 @@ def test_inplace_window_update_general_maps():
     assert_close(got, want, RTOL["f32"], "general in place via " + var)
 
 
-@pytest.mark.parametrize("case", ["options", "stencil3d", "inplace_stencil2d", "weather_cnn"])
+@pytest.mark.parametrize("case", ["options", "stencil3d", "inplace_stencil2d", "weather_cnn", "particle_cnn"])
 def test_graph_captured_inference_replays(case):
     """hpacml_infer captured in a HIP graph and
     replayed several times, with eager work and synchronisations between the
-    replays: every replay's outputs equal the eager call's bit for bit."""
+    replays: every replay's outputs equal the eager call's bit for bit (the
+    frame stack: conv + pool, split-K products, the closing kernel)."""
     import torch
     if case == "weather_cnn":
         w = wl.make_cnn("weather_cnn", (40, 130))
+        model = api.CnnModel(w.model)
+    elif case == "particle_cnn":
+        w = wl.make_cnn("particle_cnn", "small")
         model = api.CnnModel(w.model)
     else:
         w = wl.make({"inplace_stencil2d": "stencil2d"}.get(case, case),
