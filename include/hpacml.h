@@ -124,7 +124,12 @@ typedef struct hpacml_model_s hpacml_model;
  *   dir: HPACML_TO or HPACML_FROM.  A FROM map must use one slice with one
  *        element per dimension (each point writes one element per target);
  *        otherwise HPACML_E_UNSUPPORTED.  CLAMP with a nonzero offset on a FROM
- *        map is HPACML_E_INVAL (two points would write one element).
+ *        map is HPACML_E_INVAL (two points would write one element).  A FROM
+ *        map whose strides could send two sweep points to one element of a
+ *        target (a zero stride over a swept dimension, or strides that fold
+ *        the sweep onto itself) is HPACML_E_ALIAS: the swept dimensions,
+ *        taken by increasing stride, must each have a stride larger than the
+ *        element distance the finer ones can span.
  *   bnd: [rank] boundary modes. */
 hpacml_status hpacml_map_validate(const hpacml_functor *f, int32_t dir,
                                   const hpacml_array *targets, int32_t n_targets,
@@ -175,7 +180,7 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims,
 void hpacml_model_destroy(hpacml_model *m);
 
 /* ---- convolutional surrogates --------------------------------------------
- * The models the paper searches for image-shaped regions (Table VI:
+ * The models the paper searches for image-shaped regions (Table IV:
  * MiniWeather's one or two convolution layers of 4-8 channels, ParticleFilter's
  * convolution, max-pool and fully connected layers) run on the composed input
  * tensor seen as S images: the last two sweep dimensions of the `to` map are
@@ -333,7 +338,9 @@ hpacml_status hpacml_region_samples(const hpacml_region *region, int64_t *n_samp
 
 /* Copies the first n samples to HOST buffers (any may be NULL):
  * inputs [n][points(in)][F_in], outputs [n][points(out)][F_out], times_ms [n].
- * Waits for the region's work.  n > samples collected: HPACML_E_RANGE. */
+ * Waits until the records of those samples are complete, on whatever stream
+ * each was collected (an event recorded after each sample's output record),
+ * then copies.  n > samples collected: HPACML_E_RANGE. */
 hpacml_status hpacml_region_read(const hpacml_region *region, int64_t n, float *inputs, float *outputs,
                                  float *times_ms);
 

@@ -91,6 +91,8 @@ def lib():
             L = C.CDLL(_LIB)
             P = C.POINTER
             L.or_num_threads.restype = C.c_int
+            L.or_set_num_threads.argtypes = [C.c_int]
+            L.or_set_num_threads.restype = None
             L.or_bf16_bits.argtypes = [P(C.c_float), P(C.c_uint16), C.c_int64]
             L.or_map_points.argtypes = [P(_Map)]
             L.or_map_points.restype = C.c_int64
@@ -114,6 +116,12 @@ def lib():
 
 def num_threads() -> int:
     return lib().or_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads used by later oracle calls (timing only: every result is
+    independent of the thread count)."""
+    lib().or_set_num_threads(int(n))
 
 
 def _ptr(a, ct):

@@ -21,7 +21,7 @@
  *      paragraph);
  *   5. collect mode records the mapped values instead (Sec. III-A-2, IV-B);
  *   6. convolutional surrogates (the MiniWeather and ParticleFilter model
- *      spaces of Table VI: convolution, max-pool and fully connected layers)
+ *      spaces of Table IV: convolution, max-pool and fully connected layers)
  *      run on the composed tensor seen as images: the last two sweep
  *      dimensions are the image rows and columns, the features its channels.
  *
@@ -97,6 +97,17 @@ int or_num_threads(void)
     return omp_get_max_threads();
 #else
     return 1;
+#endif
+}
+
+/* Threads of later parallel loops (timing runs only; results do not depend on it). */
+void or_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0)
+        omp_set_num_threads(n);
+#else
+    (void)n;
 #endif
 }
 

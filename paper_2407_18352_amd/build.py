@@ -30,7 +30,7 @@ def _hipcc() -> str:
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-function", "-I", INCLUDE, "-I", CSRC]
 # packed fp32 VALU forms are kept out of the generated code on purpose
 DEVICE = ["-x", "hip", "--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang",
-          "-packed-fp32-ops", "-munsafe-fp-atomics"]
+          "-packed-fp32-ops"]
 
 
 def build(verbose: bool = False) -> str:

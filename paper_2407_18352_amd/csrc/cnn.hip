@@ -1,4 +1,4 @@
-// Convolutional surrogates on the composed tensor seen as images (Table VI
+// Convolutional surrogates on the composed tensor seen as images (Table IV
 // model spaces: convolutions of a few channels for MiniWeather; convolution,
 // max-pool and fully connected layers for ParticleFilter).
 //

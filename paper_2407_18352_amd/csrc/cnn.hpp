@@ -1,4 +1,4 @@
-// Convolutional surrogates (the image-shaped model spaces of Table VI):
+// Convolutional surrogates (the image-shaped model spaces of Table IV):
 // host plan, the layer-by-layer kernels and the fused convolution-stack
 // kernel.
 #pragma once

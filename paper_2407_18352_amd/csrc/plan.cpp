@@ -21,6 +21,42 @@ int64_t pos_mod(int64_t x, int64_t n) {
     return r < 0 ? r + n : r;
 }
 
+// Sufficient test that distinct sweep points address distinct elements of a
+// target.  Along dimension d the resolved coordinates of the points are
+// distinct values in [0, extent) (a periodic shift permutes them, a clamped
+// `from` map has no offset), spanning at most `span_d`: (count-1)*step without
+// a wrap, extent-1 with one.  Visiting the swept dimensions by increasing
+// stride, each stride must exceed the largest element distance the finer
+// dimensions can produce, sum(stride * span); then two points that differ in
+// their coarsest differing dimension cannot meet.  Row-major and strided views
+// pass; a zero stride or a stride that folds the sweep does not.
+bool injective_sweep(const MapPlan &p, const hpacml_array &a) {
+    struct Dim {
+        int64_t stride, span;
+    };
+    Dim dims[HPACML_MAX_RANK];
+    int n = 0;
+    for (int d = 0; d < p.rank; ++d) {
+        if (p.count[d] <= 1)
+            continue;
+        int64_t span = (p.count[d] - 1) * p.step[d];
+        const int64_t first = p.start[d] + p.raw[d], last = first + span;   // slice 0 of the functor
+        if (p.bnd[d] == HPACML_BND_PERIODIC && (first < 0 || last >= p.extent[d]))
+            span = p.extent[d] - 1;
+        dims[n++] = {a.stride[d], span};
+    }
+    std::sort(dims, dims + n, [](const Dim &x, const Dim &y) { return x.stride < y.stride; });
+    int64_t reach = 0;   // largest element distance of the finer dimensions
+    for (int i = 0; i < n; ++i) {
+        if (dims[i].stride <= reach)
+            return false;
+        int64_t term;
+        if (!mul_ok(dims[i].stride, dims[i].span, &term) || !add_ok(reach, term, &reach))
+            return false;
+    }
+    return true;
+}
+
 }  // namespace
 
 hpacml_status build_map_plan(const hpacml_functor *f, int32_t dir, const hpacml_array *targets,
@@ -168,6 +204,14 @@ hpacml_status build_map_plan(const hpacml_functor *f, int32_t dir, const hpacml_
         for (int d = 0; d < R; ++d)
             if (p.bnd[d] == HPACML_BND_CLAMP && f->slices[0].lo[d] != 0)
                 return HPACML_E_INVAL;
+
+    // a `from` map writes one element per point and target, so two sweep
+    // points must never land on one element: stride-0 views (broadcasts) and
+    // strides that fold the sweep onto itself are refused
+    if (dir == HPACML_FROM && npts > 1)
+        for (int t = 0; t < n_targets; ++t)
+            if (!injective_sweep(p, targets[t]))
+                return HPACML_E_ALIAS;
 
     // wrapping: per-target base and strides, element extents
     p.base.resize(n_targets);

@@ -28,7 +28,8 @@ struct hpacml_region_s {
     int32_t f_in = 0, f_out = 0;
     int64_t capacity = 0, n = 0;
     float *in_rec = nullptr, *out_rec = nullptr;   // device [capacity][points][F]
-    std::vector<hipEvent_t> ev;                    // [2 * capacity]: around each accurate path
+    std::vector<hipEvent_t> ev;                    // [3 * capacity]: around each accurate path, and
+                                                   // after the sample's output record
     std::mutex mu;
 };
 
@@ -110,7 +111,7 @@ hpacml_status hpacml_region_create(const hpacml_model *model, const hpacml_map *
                 return hip_status(e);
             }
         }
-        r->ev.assign((size_t)(2 * r->capacity), nullptr);
+        r->ev.assign((size_t)(3 * r->capacity), nullptr);
         *region = r;
         return HPACML_OK;
     } catch (const std::bad_alloc &) {
@@ -142,12 +143,14 @@ hpacml_status hpacml_region_run(hpacml_region *r, int32_t cond, int32_t enabled,
     const int64_t k = r->n;
     float *in_slot = r->in_rec ? r->in_rec + (size_t)k * r->points * r->f_in : nullptr;
     float *out_slot = r->out_rec ? r->out_rec + (size_t)k * r->points_out * r->f_out : nullptr;
-    hipEvent_t &e0 = r->ev[2 * k], &e1 = r->ev[2 * k + 1];
+    hipEvent_t &e0 = r->ev[3 * k], &e1 = r->ev[3 * k + 1], &e2 = r->ev[3 * k + 2];
     hipError_t he = hipSuccess;
     if (!e0)
         he = hipEventCreate(&e0);
     if (he == hipSuccess && !e1)
         he = hipEventCreate(&e1);
+    if (he == hipSuccess && !e2)
+        he = hipEventCreateWithFlags(&e2, hipEventDisableTiming);
     if (he != hipSuccess)
         return hip_status(he);
     // inputs before the accurate path writes anything, outputs after it
@@ -162,6 +165,9 @@ hpacml_status hpacml_region_run(hpacml_region *r, int32_t cond, int32_t enabled,
     s = r->points_out ? record(r->out, out_slot, r->f_out, stream) : HPACML_OK;
     if (s != HPACML_OK)
         return s;
+    // the sample is complete once this event has passed (read waits on it)
+    if ((he = hipEventRecord(e2, st)) != hipSuccess)
+        return hip_status(he);
     r->n = k + 1;
     return HPACML_OK;
 }
@@ -180,15 +186,17 @@ hpacml_status hpacml_region_read(const hpacml_region *r, int64_t n, float *input
     if (n > r->n)
         return HPACML_E_RANGE;
     hipError_t e = hipSuccess;
-    if (inputs && n && r->points)
+    // every sample's records complete, whatever stream the region ran on
+    // (a blocking copy is ordered after the null stream only)
+    for (int64_t k = 0; e == hipSuccess && k < n; ++k)
+        e = hipEventSynchronize(r->ev[3 * k + 2]);
+    if (e == hipSuccess && inputs && n && r->points)
         e = hipMemcpy(inputs, r->in_rec, (size_t)n * r->points * r->f_in * sizeof(float), hipMemcpyDeviceToHost);
     if (e == hipSuccess && outputs && n && r->points_out)
         e = hipMemcpy(outputs, r->out_rec, (size_t)n * r->points_out * r->f_out * sizeof(float),
                       hipMemcpyDeviceToHost);
     for (int64_t k = 0; e == hipSuccess && times_ms && k < n; ++k) {
-        e = hipEventSynchronize(r->ev[2 * k + 1]);
-        if (e == hipSuccess)
-            e = hipEventElapsedTime(&times_ms[k], r->ev[2 * k], r->ev[2 * k + 1]);
+        e = hipEventElapsedTime(&times_ms[k], r->ev[3 * k], r->ev[3 * k + 1]);
     }
     return hip_status(e);
 }

@@ -280,7 +280,7 @@ def edge_rows_2d(ny: int, nx: int) -> np.ndarray:
     return np.asarray(sorted(cells), np.int64)
 
 
-# ---- convolutional surrogates (Table VI model spaces) ----------------------
+# ---- convolutional surrogates (Table IV model spaces) ----------------------
 # * ``weather_cnn``  MiniWeather-like: 4 periodic state fields on an ny x nx
 #   grid (sums of sinusoids, as ``stencil2d``); conv 5x5 4 -> 8 (circular,
 #   ReLU), conv 3x3 8 -> 4 (circular); kernel sizes and channels from the

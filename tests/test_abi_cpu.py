@@ -159,6 +159,55 @@ def test_map_validation_errors(case, status):
     assert api.validate_map(spec, arrays, direction, nf)[0] == status
 
 
+def _brute_injective(spec, shape, strides):
+    """Do the sweep points of a one-element `from` functor land on distinct
+    element indices?  (Enumerates every point; tiny shapes only.)"""
+    import itertools
+    import numpy as np
+    start, stop, step = spec["sweep"]
+    lo = spec["slices"][0][0]
+    seen = set()
+    for pt in itertools.product(*[range(a, b, c) for a, b, c in zip(start, stop, step)]):
+        q = []
+        for d, x in enumerate(pt):
+            y = x + lo[d]
+            if spec["bnd"][d] == wl.PERIODIC:
+                y %= shape[d]
+            q.append(y)
+        e = int(np.dot(q, strides))
+        if e in seen:
+            return False
+        seen.add(e)
+    return True
+
+
+@pytest.mark.parametrize("shape, strides, sweep, lo, bnd", [
+    ((8,), (0,), ((0,), (8,), (1,)), (0,), [0]),                         # broadcast view
+    ((4, 4), (1, 1), ((0, 0), (4, 4), (1, 1)), (0, 0), [0, 0]),          # strides {1, 1} fold the sweep
+    ((4, 4), (0, 1), ((0, 0), (4, 4), (1, 1)), (0, 0), [0, 0]),          # a zero stride on a swept dimension
+    ((3, 5), (2, 1), ((0, 0), (3, 5), (1, 1)), (0, 0), [0, 0]),          # rows overlap by 3 elements
+    ((3, 5), (2, 1), ((0, 0), (3, 5), (1, 2)), (0, 0), [0, 0]),          # even columns: 0,2,4 then 2,4,6
+    ((3, 5), (5, 1), ((0, 0), (3, 5), (1, 1)), (0, 0), [0, 0]),          # row-major: fine
+    ((3, 5), (1, 3), ((0, 0), (3, 5), (1, 1)), (0, 0), [0, 0]),          # column-major: fine
+    ((3, 5), (6, 1), ((0, 0), (3, 5), (1, 1)), (0, 0), [0, 0]),          # padded rows: fine
+    ((3, 5), (2, 1), ((0, 0), (3, 2), (1, 1)), (0, 0), [0, 0]),          # two columns of overlapping rows: fine
+    ((3, 5), (0, 1), ((1, 0), (2, 5), (1, 1)), (0, 0), [0, 0]),          # zero stride on an unswept dimension: fine
+    ((6,), (1,), ((0,), (6,), (1,)), (2,), [wl.PERIODIC]),                # periodic shift: a permutation
+    ((3, 4), (3, 1), ((0, 0), (3, 4), (1, 1)), (0, 1), [0, wl.PERIODIC]), # wrap spans the whole row: folds
+])
+def test_from_map_must_be_one_to_one(shape, strides, sweep, lo, bnd):
+    """A `from` map whose strides could send two sweep points to one element
+    is refused (E_ALIAS); one that cannot is accepted.  The expectation is
+    brute force over every point, for the cases where the library's
+    sufficient test is exact."""
+    spec = {"rank": len(shape), "slices": [(lo, (1,) * len(shape))], "sweep": sweep, "bnd": bnd}
+    st = api.validate_map(spec, [_arr(shape, strides=list(strides))], _abi.FROM)[0]
+    want = _abi.OK if _brute_injective(spec, shape, strides) else _abi.E_ALIAS
+    assert st == want
+    # a `to` map may read one element from several points
+    assert api.validate_map(spec, [_arr(shape, strides=list(strides))], _abi.TO)[0] == _abi.OK
+
+
 def test_offsets_beyond_extent_wrap():
     spec = {"rank": 1, "slices": [((-20,), (3,))], "sweep": ((0,), (5,), (1,)), "bnd": [wl.PERIODIC]}
     assert api.validate_map(spec, [_arr((5,))], _abi.TO)[:3] == (_abi.OK, 5, 3)

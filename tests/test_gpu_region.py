@@ -235,3 +235,38 @@ def test_predicated_region_over_an_in_place_convolutional_step():
         assert np.array_equal(ins[j].view(np.uint32), recs[2 * j]), j
         assert np.array_equal(outs[j].view(np.uint32), recs[2 * j + 1]), j
     assert np.all(t > 0)
+
+
+def test_read_waits_for_a_region_run_on_a_side_stream():
+    """A collecting region run on a non-blocking stream, read back with no
+    synchronisation by the caller: the read must wait for each sample's
+    records (the accurate path here queues ~10 ms of matrix products before it
+    writes the outputs, so a read that did not wait would see stale data)."""
+    import torch
+    s = Setup(n=1 << 18)
+    side = torch.cuda.Stream()
+    a = torch.randn(4096, 4096, device="cuda")
+    pat = [torch.from_numpy(s.pattern(k)).cuda() for k in range(2)]
+    expect_in = oracle.collect(s.w.in_spec, s.host_inputs())
+    torch.cuda.synchronize()
+
+    def slow(k):
+        def run(stream_handle):
+            st = torch.cuda.ExternalStream(stream_handle)
+            with torch.cuda.stream(st):
+                x = a
+                for _ in range(10):
+                    x = (x @ a) * (1.0 / 64)
+                s.outs[0].copy_(pat[k] + 0 * x[0, 0])
+        return run
+
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_COLLECT, capacity=2)
+    with torch.cuda.stream(side):
+        for k in range(2):
+            r.run(slow(k), stream=side)
+    ins, outs, t = r.read()          # no synchronize before this
+    for k in range(2):
+        assert np.array_equal(ins[k].view(np.uint32), expect_in), k
+        assert np.array_equal(outs[k, :, 0], s.pattern(k)), k
+    assert np.all(t > 0)
+    torch.cuda.synchronize()

@@ -1,5 +1,5 @@
 """Pins of the oracle's convolutional surrogates (the MiniWeather and
-ParticleFilter model spaces of Table VI), each against something other than
+ParticleFilter model spaces of Table IV), each against something other than
 the oracle's own formula:
 
 * random stacks of convolution (every padding mode, even and odd windows,
