@@ -30,6 +30,7 @@
 #ifndef HPACML_H
 #define HPACML_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -357,6 +358,30 @@ hpacml_status hpacml_region_reset(hpacml_region *region);
 /* Frees a region and its sink (not its maps or model).  NULL-safe.
  * Synchronise the streams that use it first. */
 void hpacml_region_destroy(hpacml_region *region);
+
+/* ---- inference without allocation ---------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.
+ *
+ * hpacml_infer_noalloc computes exactly what hpacml_infer computes, with the
+ * same kernels, and allocates nothing (no hipMalloc / hipFree, no host heap).
+ * Where hpacml_infer would copy the inputs into the `to` map's snapshot
+ * record first (outputs that may overwrite inputs other points still read),
+ * this entry point puts that record in a fixed scratch array of
+ * HPACML_NOALLOC_SCRATCH_BYTES per device, held until the process ends.
+ *   HPACML_E_RANGE        the record (points x F_in x 4 bytes) is larger than
+ *                         the scratch array; nothing is enqueued.
+ *   HPACML_E_UNSUPPORTED  convolutional models, and in-place inferences whose
+ *                         maps or model take the general kernel (they need
+ *                         device tables of their own).
+ * Other statuses as hpacml_infer.  Asynchronous on `stream`.  Every call on
+ * one device shares that device's scratch array: calls that overlap on one
+ * device (on different streams) race; calls ordered on one stream do not.
+ * The array keeps the last call's record, and every call overwrites the part
+ * it reads before reading it. */
+#define HPACML_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+hpacml_status hpacml_infer_noalloc(const hpacml_model *model, const hpacml_map *in,
+                                   const hpacml_map *out, void *stream);
 
 /* Name of the kernel hpacml_infer would launch for these handles (a static
  * string, prefixed "snapshot+" when the inputs are copied first), or NULL

@@ -62,6 +62,7 @@ SIGNATURES = {
                                       _P(C.c_int32), C.c_int32, _P(C.c_void_p)]),
     "hpacml_model_destroy": (None, [C.c_void_p]),
     "hpacml_infer": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
+    "hpacml_infer_noalloc": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
     "hpacml_collect": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p]),
     "hpacml_collect_pair": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_int64,
                                       C.c_void_p]),

@@ -213,6 +213,26 @@ DevMap make_devmap(const MapPlan &p, const FeatureEntry *feat_dev, float *const 
     return m;
 }
 
+// Division by m->count[d]: n / c == (n * magic) >> (31 + l) for n < 2^31,
+// l = ceil(log2 c); false when the multiplier does not fit or a probe fails.
+bool set_div_magic(Map32 *m, int d) {
+    const uint64_t dv = (uint64_t)m->count[d];
+    int l = 0;
+    while ((uint64_t(1) << l) < dv)
+        ++l;
+    const uint64_t magic = ((uint64_t(1) << (31 + l)) + dv - 1) / dv;
+    if (magic > UINT32_MAX)
+        return false;
+    m->magic[d] = (uint32_t)magic;
+    m->shift[d] = 31 + l;
+    const uint32_t probes[6] = {0u, (uint32_t)dv - 1u, (uint32_t)dv, (uint32_t)(2 * dv - 1), (uint32_t)INT32_MAX,
+                                (uint32_t)INT32_MAX - 1u};
+    for (uint32_t n : probes)
+        if ((uint32_t)(((uint64_t)n * m->magic[d]) >> m->shift[d]) != n / (uint32_t)dv)
+            return false;
+    return true;
+}
+
 bool make_map32(const MapPlan &p, Map32 *out) {
     const int64_t lim = INT32_MAX;
     Map32 m{};
@@ -242,21 +262,8 @@ bool make_map32(const MapPlan &p, Map32 *out) {
         m.bnd[d] = p.bnd[d];
         m.omin[d] = p.omin[d];
         m.omax[d] = p.omax[d];
-        // n / d == (n * magic) >> (31 + l) for n < 2^31, l = ceil(log2 d)
-        const uint64_t dv = (uint64_t)m.count[d];
-        int l = 0;
-        while ((uint64_t(1) << l) < dv)
-            ++l;
-        const uint64_t magic = ((uint64_t(1) << (31 + l)) + dv - 1) / dv;
-        if (magic > UINT32_MAX)
+        if (!set_div_magic(&m, d))
             return false;
-        m.magic[d] = (uint32_t)magic;
-        m.shift[d] = 31 + l;
-        const uint32_t probes[6] = {0u, (uint32_t)dv - 1u, (uint32_t)dv, (uint32_t)(2 * dv - 1),
-                                    (uint32_t)INT32_MAX, (uint32_t)INT32_MAX - 1u};
-        for (uint32_t n : probes)
-            if ((uint32_t)(((uint64_t)n * m.magic[d]) >> m.shift[d]) != n / (uint32_t)dv)
-                return false;
     }
     *out = m;
     return true;
@@ -915,6 +922,71 @@ const char *snapshot_name(const char *kernel) {
 
 }  // namespace
 
+namespace {
+
+// ---- scratch for inference without allocation ------------------------------
+// A fixed array per device holds the snapshot record of in-place inferences
+// made through hpacml_infer_noalloc.  In host code `scratch` names a host-side
+// stand-in: its device address comes from hipGetSymbolAddress, taken once per
+// device (with that device current) and kept; only that address is ever
+// passed to kernels.  Every call on a device shares the array, so calls that
+// overlap on one device (different streams) race.
+constexpr size_t kNoallocScratchBytes = HPACML_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+hpacml_status scratch_address(int device, void **out) {
+    if (device < 0 || device >= kMaxDevices)
+        return HPACML_E_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || p == nullptr) {
+            (void)hipGetLastError();
+            return HPACML_E_DEVICE;
+        }
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
+    return HPACML_OK;
+}
+
+// The feature-major record [F][B] at `buf` as a rank-1 pointwise map in the
+// 32-bit form: target f is buf + f * B, every feature reads its point.  Built
+// without any allocation (no MapPlan); false when it does not fit the form.
+bool record_map32(int64_t B, int32_t F, float *buf, Map32 *m, FeatTable32 *t) {
+    if (B < 1 || B >= INT32_MAX / 3 || F < 1 || F > kTableMaxF)
+        return false;
+    Map32 r{};
+    r.rank = 1;
+    r.n_features = F;
+    r.n_targets = F;
+    r.n_points = (int32_t)B;
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        r.count[d] = d == 0 ? (int32_t)B : 1;
+        r.start[d] = 0;
+        r.step[d] = 1;
+        r.extent[d] = d == 0 ? (int32_t)B : 1;
+        r.stride[d] = d == 0 ? 1 : 0;
+        r.bnd[d] = HPACML_BND_NONE;
+        r.omin[d] = r.omax[d] = 0;
+        if (!set_div_magic(&r, d))
+            return false;
+    }
+    for (int f = 0; f < kTableMaxF; ++f) {
+        t->fptr[f] = buf + (size_t)(f < F ? f : F - 1) * B;
+        t->raw8[f] = 0;
+    }
+    *m = r;
+    return true;
+}
+
+}  // namespace
+
 const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out) {
     bool snapshot = false;
     if (check_infer(model, in, out, &snapshot) != HPACML_OK)
@@ -956,6 +1028,60 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
     case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, in->tab, out->tab, model->bf16, st); break;
     default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
     }
+    return hip_status(e);
+}
+
+hpacml_status hpacml_infer_noalloc(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out,
+                                   void *stream) {
+    bool snapshot = false;
+    hpacml_status s = check_infer(model, in, out, &snapshot);
+    if (s != HPACML_OK)
+        return s;
+    if (model->cnn)
+        return HPACML_E_UNSUPPORTED;
+    hipStream_t st = (hipStream_t)stream;
+    const bool fast = in->t32 && out->t32;
+    if (!snapshot) {
+        // disjoint (or element-for-element) maps: the kernels read the
+        // application arrays directly and need no scratch
+        if (in->plan.n_points == 0)
+            return HPACML_OK;
+        hipError_t e;
+        switch (fast ? model->variant : Variant::Generic) {
+        case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, in->tab, out->tab, model->f32, st); break;
+        case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, in->tab, out->tab, model->bf16, st); break;
+        default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
+        }
+        return hip_status(e);
+    }
+    // outputs that may overwrite inputs: the snapshot record goes to the
+    // device's scratch array, read back through a map built on the host
+    if (!fast || model->variant == Variant::Generic)
+        return HPACML_E_UNSUPPORTED;
+    const int64_t B = in->plan.n_points;
+    const int32_t F = in->plan.n_features;
+    if ((uint64_t)B * (uint64_t)F * sizeof(float) > kNoallocScratchBytes)
+        return HPACML_E_RANGE;
+    if (B == 0)
+        return HPACML_OK;
+    void *ptr = nullptr;
+    s = scratch_address(model->device, &ptr);
+    if (s != HPACML_OK)
+        return s;
+    Map32 rm{};
+    FeatTable32 rt{};
+    if (!record_map32(B, F, (float *)ptr, &rm, &rt))
+        return HPACML_E_UNSUPPORTED;
+    CollectJob32 j = collect32_job(in->plan, in->m32, in->tab, in->tab_dev, (uint32_t *)ptr, 1);
+    j.dense = 0;
+    j.fs = B;   // feature-major [F][B]
+    hipError_t e = launch_collect32(&j, 1, st);
+    if (e != hipSuccess)
+        return hip_status(e);
+    if (model->variant == Variant::F32)
+        e = launch_mlp_f32(rm, out->m32, rt, out->tab, model->f32, st);
+    else
+        e = launch_mlp_bf16(rm, out->m32, rt, out->tab, model->bf16, st);
     return hip_status(e);
 }
 
