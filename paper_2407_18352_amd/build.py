@@ -33,13 +33,18 @@ DEVICE = ["-x", "hip", "--offload-arch=" + ARCH, "-Xclang", "-target-feature", "
           "-packed-fp32-ops"]
 
 
+# the register-resident bf16 kernel keeps its activations in accumulation
+# registers as MFMA B operands; results and C operands go to vector registers
+PER_FILE = {"mlp_bf16r.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def build(verbose: bool = False) -> str:
     hipcc = _hipcc()
     os.makedirs(BUILD, exist_ok=True)
     jobs = []
     for src in sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp"))):
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-        cmd = [hipcc] + COMMON + (DEVICE if src.endswith(".hip") else ["-x", "c++"])
+        cmd = [hipcc] + COMMON + (DEVICE if src.endswith(".hip") else ["-x", "c++"]) + PER_FILE.get(os.path.basename(src), [])
         cmd += ["-c", src, "-o", obj]
         jobs.append((cmd, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
     objs = []

@@ -36,7 +36,7 @@ struct hpacml_map_s {
     mutable hpacml_map *snap_map = nullptr;
 };
 
-enum class Variant { Generic, F32, BF16 };
+enum class Variant { Generic, F32, BF16, BF16R };
 
 struct hpacml_model_s {
     int32_t n_layers = 0, compute = 0;
@@ -49,6 +49,8 @@ struct hpacml_model_s {
     F32Packed f32{};
     uint16_t *bf16_frags = nullptr;  // packed fragments of the bf16 kernel
     BF16Packed bf16{};
+    uint8_t *bf16r_buf = nullptr;    // weight stream, output fragments, biases of the register-resident bf16 kernel
+    BF16RPacked bf16r{};
     // convolutional models
     bool cnn = false;
     CnnPlan cnnp;
@@ -468,6 +470,7 @@ void hpacml_model_destroy(hpacml_model *m) {
     (void)hipFree(m->gen_buf);
     (void)hipFree(m->f32_img);
     (void)hipFree(m->bf16_frags);
+    (void)hipFree(m->bf16r_buf);
     (void)hipFree(m->cnn_buf);
     (void)hipFree(m->fused_buf);
     (void)hipFree(m->ws);
@@ -550,6 +553,21 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
             m->f32.lds_bytes = (int32_t)(img.size() * sizeof(float));
             m->f32.image = m->f32_img;
             m->variant = Variant::F32;
+        } else if (bf16r_supported(n_layers, dims, act, compute)) {
+            std::vector<uint8_t> buf;
+            size_t off_w3 = 0, off_bias = 0;
+            bf16r_pack(n_layers, dims, W, b, buf, &off_w3, &off_bias, &m->bf16r);
+            s = upload(&m->bf16r_buf, buf.data(), buf.size());
+            if (s != HPACML_OK) {
+                hpacml_model_destroy(m);
+                return s;
+            }
+            for (int l = 0; l < n_layers; ++l)
+                m->bf16r.act[l] = act[l];
+            m->bf16r.stream = m->bf16r_buf;
+            m->bf16r.w3 = m->bf16r_buf + off_w3;
+            m->bf16r.bias = (const float *)(m->bf16r_buf + off_bias);
+            m->variant = Variant::BF16R;
         } else if (bf16_fast_supported(n_layers, dims, compute)) {
             std::vector<uint16_t> frags;
             bf16_pack(n_layers, dims, W, b, frags, &m->bf16);
@@ -893,6 +911,7 @@ const char *kernel_name(const hpacml_model *model, bool fast) {
     switch (fast ? model->variant : Variant::Generic) {
     case Variant::F32: return f32_variant_name(model->f32);
     case Variant::BF16: return bf16_variant_name(model->bf16);
+    case Variant::BF16R: return bf16r_variant_name(model->bf16r);
     default: return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
     }
 }
@@ -1026,6 +1045,7 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
     switch (fast ? model->variant : Variant::Generic) {
     case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, in->tab, out->tab, model->f32, st); break;
     case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, in->tab, out->tab, model->bf16, st); break;
+    case Variant::BF16R: e = launch_mlp_bf16r(in->m32, out->m32, in->tab, out->tab, model->bf16r, st); break;
     default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
     }
     return hip_status(e);
@@ -1050,6 +1070,7 @@ hpacml_status hpacml_infer_noalloc(const hpacml_model *model, const hpacml_map *
         switch (fast ? model->variant : Variant::Generic) {
         case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, in->tab, out->tab, model->f32, st); break;
         case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, in->tab, out->tab, model->bf16, st); break;
+        case Variant::BF16R: e = launch_mlp_bf16r(in->m32, out->m32, in->tab, out->tab, model->bf16r, st); break;
         default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
         }
         return hip_status(e);
@@ -1080,6 +1101,8 @@ hpacml_status hpacml_infer_noalloc(const hpacml_model *model, const hpacml_map *
         return hip_status(e);
     if (model->variant == Variant::F32)
         e = launch_mlp_f32(rm, out->m32, rt, out->tab, model->f32, st);
+    else if (model->variant == Variant::BF16R)
+        e = launch_mlp_bf16r(rm, out->m32, rt, out->tab, model->bf16r, st);
     else
         e = launch_mlp_bf16(rm, out->m32, rt, out->tab, model->bf16, st);
     return hip_status(e);

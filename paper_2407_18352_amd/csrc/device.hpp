@@ -135,15 +135,22 @@ __device__ __forceinline__ const float *feature_ptr(const DevMap &m, const int64
     return m.base[e.target] + idx;
 }
 
-// max(x, 0) in one v_max_f32, for x produced by arithmetic (an MFMA result):
-// such an x is never a signalling NaN, and in IEEE mode v_max_f32 returns the
-// other operand for a quiet NaN, so max(NaN, 0) = 0 as for fmaxf.  (fmaxf
-// compiles to a quieting v_max_f32 x, x before the max, twice the cost.)
+// max(x, 0) in one v_max_f32, for x produced by vector ALU arithmetic (not an
+// MFMA result: see relu_mfma): such an x is never a signalling NaN, and in
+// IEEE mode v_max_f32 returns the other operand for a quiet NaN, so
+// max(NaN, 0) = 0 as for fmaxf.  (fmaxf compiles to a quieting v_max_f32
+// x, x before the max, twice the cost.)
 __device__ __forceinline__ float relu_arith(float x) {
     float r;
     asm("v_max_f32 %0, 0, %1" : "=v"(r) : "v"(x));
     return r;
 }
+
+// max(x, 0) for x an MFMA result, as one v_med3_f32(x, 0, +inf) that the
+// compiler sees, so it keeps the wait states an MFMA's result needs before the
+// vector ALU reads it (inline assembly would bypass that check).  A NaN gives
+// 0, as for fmaxf.
+__device__ __forceinline__ float relu_mfma(float x) { return __builtin_amdgcn_fmed3f(x, 0.f, __builtin_inff()); }
 
 // Round to bf16 (nearest even, by the hardware conversion) and back to fp32.
 __device__ __forceinline__ float round_bf16(float x) {

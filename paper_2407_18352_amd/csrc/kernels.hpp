@@ -100,6 +100,37 @@ hipError_t launch_mlp_bf16(const Map32 &in, const Map32 &out, const FeatTable32 
                            const BF16Packed &pk, hipStream_t stream);
 const char *bf16_variant_name(const BF16Packed &pk);
 
+// Host bf16 helpers shared by the bf16 packers: round to nearest even (NaN
+// stays a quiet NaN), the value of a bf16 pattern, and an fp32 bias split
+// exactly into three bf16 terms (hi + mid + lo == b).
+uint16_t bf16_rne_host(float x);
+float bf16_value(uint16_t h);
+void split_bias(float b, uint16_t out[3]);
+
+// bf16 fused kernel with register-resident activations: uniform hidden width
+// H in {256, 512} (one hidden layer at 512, up to two at 256), ReLU hidden
+// layers, F_in <= 45, F_out <= 8.  Weights stream through an LDS ring.
+struct BF16RPacked {
+    int32_t hid;          // H
+    int32_t n_hidden;     // hidden-to-hidden layers (H x H)
+    int32_t ks1;          // 16-wide K-steps of the first layer
+    int32_t f_out;        // outputs
+    int32_t stages;       // 16 KB ring stages per tile of 256 points
+    int32_t act[HPACML_MAX_LAYERS];
+    const void *stream;   // device: the weight stream of one tile [stages][16][64 lanes][8 bf16]
+    const void *w3;       // device: output-layer fragments [H/32][2][64][8 bf16]
+    const float *bias;    // device: hidden biases in the accumulator layout [n_hidden][H/32][2][16]
+    float bias_out[16];
+};
+bool bf16r_supported(int n_layers, const int32_t *dims, const int32_t *act, int compute);
+// Packed buffers: stream, then w3, then bias (16-byte aligned parts); the
+// offsets of w3 and bias in bytes.
+void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
+                std::vector<uint8_t> &buf, size_t *off_w3, size_t *off_bias, BF16RPacked *pk);
+hipError_t launch_mlp_bf16r(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                            const BF16RPacked &pk, hipStream_t stream);
+const char *bf16r_variant_name(const BF16RPacked &pk);
+
 // The status hpacml_infer would return for these handles, without launching.
 hpacml_status infer_status(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out);
 

@@ -289,7 +289,7 @@ __global__ void __launch_bounds__(kThreads) mlp_bf16_kernel(Map32 in, Map32 out,
                             float v[8];
 #pragma unroll
                             for (int e = 0; e < 8; ++e)
-                                v[e] = relu_arith(acc[j][n][8 * sp + e]);
+                                v[e] = relu_mfma(acc[j][n][8 * sp + e]);
                             Hs[(p0 + 32 * n) * G::PH + 4 * (m0 + j) + 2 * sp + g] = pack8(v);
                         }
             } else {
@@ -397,6 +397,8 @@ hipError_t launch_t(const Map32 &in, const Map32 &out, const FeatTable32 &tin, c
     return hipGetLastError();
 }
 
+}  // namespace
+
 uint16_t bf16_rne_host(float x) {
     uint32_t u;
     std::memcpy(&u, &x, 4);
@@ -426,8 +428,6 @@ void split_bias(float b, uint16_t out[3]) {
     const float r2 = r1 - bf16_value(out[1]);
     out[2] = bf16_rne_host(r2);
 }
-
-}  // namespace
 
 bool bf16_fast_supported(int n_layers, const int32_t *dims, int compute) {
     if (compute != HPACML_BF16 || n_layers < 2 || n_layers > HPACML_MAX_LAYERS)

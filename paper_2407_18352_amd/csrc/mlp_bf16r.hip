@@ -1,0 +1,644 @@
+// bf16 fused region kernel with register-resident activations: gather -> MLP
+// -> scatter for wide hidden layers (H in {256, 512}), bf16 operands with
+// fp32 accumulation on v_mfma_f32_32x32x16_bf16.
+//
+// The surrogate runs per sweep point on the composed input tensor (Sec. IV-A
+// composition, Sec. IV-B inference).  Each wave owns 64 points outright and
+// keeps every activation of those points in its own registers (H x 64 bf16 =
+// 64 KB at H = 512: 256 accumulation registers, read by the MFMA as its B
+// operand), so no layer ever exchanges activations with another wave and no
+// block-wide barrier separates the layers: the epilogue of one 32-feature
+// block (bias, activation, bf16 rounding, and for the last hidden layer its
+// share of the output layer) runs on the vector ALU while the matrix core
+// works through the next block.  One wave per SIMD (512 registers).
+//
+// Every layer is computed transposed, H_out^T = W * H_in^T: A = 32 output
+// features x 16 inputs of W (one 1 KB fragment), B = 16 inputs x 32 points of
+// the activations (registers), C = 32 features x 32 points.  In the C layout
+// lane l holds point l % 32 and, in register r, feature 8 (r / 4) + 4 (l / 32)
+// + r % 4; registers 8t..8t+7, rounded to bf16, are directly the B operand of
+// K-step 2j + t of the next layer when that layer's weight columns are
+// permuted accordingly at pack time.  The first layer's bias rides in three
+// bf16 columns of its zero-padded K; the hidden layers' biases (fp32) are
+// added in the epilogue.
+//
+// The weights stream from L2 once per tile of 256 points (4 waves x 64) into
+// a ring of 16 KB stages in LDS with direct global-to-LDS loads, each wave
+// loading a quarter of every stage; all four waves read every fragment of it
+// (each fragment feeds one MFMA per 32 points of the wave).  A stage is
+// published by a wait for the wave's own loads and one barrier, taken a few
+// fragments before the stage is needed.  The inputs of tile t + 2 are
+// gathered during tile t through the `to` map, one direct load per feature
+// and wave per stage, into a second LDS buffer, so their latency (window rows
+// and planes that miss the caches) has a whole tile to pass.  The direct loads
+// are issued as inline assembly the compiler does not see: seeing them, it
+// would make every LDS read wait for all of them (it cannot tell one ring
+// slot from another); their completion is this kernel's own count of
+// vector-memory loads, and the barriers that publish their data are
+// assembly with a memory clobber, so no LDS access moves across one.
+#include <type_traits>
+
+#include "kernels.hpp"
+
+namespace hpacml {
+
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));   // one fragment in registers
+
+constexpr int kW = 4;                  // waves per block, one per SIMD
+constexpr int kThreads = 64 * kW;
+constexpr int kP = 64;                 // points per wave: two 32-point n-blocks
+constexpr int kT = kW * kP;            // points per tile
+constexpr int kFrag = 1024;            // one MFMA operand fragment: 64 lanes x 16 bytes
+constexpr int kSF = 16;                // fragments per ring stage
+constexpr int kStage = kSF * kFrag;    // 16 KB
+constexpr int kPd = 4;                 // fragment reads in flight ahead of their use
+constexpr int kR = 8;                  // fragments held in registers (> kPd, divides the layers' fragment counts)
+constexpr int kSync = kSF - kPd;       // fragment of a stage at which the next one is published
+constexpr int kNS = 4;                 // ring stages in LDS
+constexpr int kD = kNS - 1;            // stages loaded ahead
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// two fp32 -> packed bf16 pair (round to nearest even), one instruction
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+    const floatx2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// registers 8t..8t+7 of a C fragment, plus the bias, after ReLU (max(x, 0),
+// a NaN giving 0), as a B fragment of the next layer.  Plain fmaxf, so the
+// compiler sees the vector ALU reading the MFMA's result and keeps the wait
+// states that read requires.
+__device__ __forceinline__ u32x4 to_b(const floatx16 &c, int t, const floatx16 &bias) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        v[e] = __builtin_fmaxf(c[8 * t + e] + bias[8 * t + e], 0.f);
+    return u32x4{pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])};
+}
+__device__ __forceinline__ u32x4 to_b(const floatx16 &c, int t) {
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+        v[e] = relu_mfma(c[8 * t + e]);
+    return u32x4{pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])};
+}
+
+// Keep an activation fragment in an accumulation register: the MFMA reads
+// its B operand from there directly, which leaves the vector registers to
+// everything the vector ALU touches (the activations of 64 points fill 256).
+__device__ __forceinline__ u32x4 to_agpr(u32x4 v) {
+    asm volatile("" : "+a"(v));
+    return v;
+}
+
+// wait until at most N vector-memory loads of this wave are outstanding
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// block barrier that no memory access (LDS included) moves across
+__device__ __forceinline__ void block_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// direct global -> LDS loads (lane i's bytes land at lds + i * bytes; `lds`
+// is wave-uniform); M0 is saved and restored around its use
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds) {
+    uint32_t save;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(save)
+                 : "v"(g), "s"(lds)
+                 : "memory");
+}
+__device__ __forceinline__ void dma4(const void *g, uint32_t lds) {
+    uint32_t save;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(save)
+                 : "v"(g), "s"(lds)
+                 : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// compile-time loop: fn(std::integral_constant<int, i>) for i in [B, E)
+template <int B, int E, typename Fn>
+__device__ __forceinline__ void static_for(Fn &&fn) {
+    if constexpr (B < E) {
+        fn(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(fn);
+    }
+}
+
+// Tile geometry and the weight stream of one tile
+template <int H, int NH, int KS1>
+struct RGeo {
+    static constexpr int NMB = H / 32;                    // 32-feature m-blocks
+    static constexpr int KS = H / 16;                     // K-steps of a hidden layer
+    static constexpr int L1F = NMB * KS1;                 // first-layer fragments
+    static constexpr int L1S = (L1F + kSF - 1) / kSF;     // ... in whole stages
+    static constexpr int HF = NMB * KS;                   // fragments of a hidden layer
+    static constexpr int ST = L1S + NH * HF / kSF;        // stages per tile
+    static_assert(HF % kSF == 0, "hidden layers are whole stages");
+    static_assert(KS % kR == 0 && (L1S * kSF) % kR == 0, "fragment registers aligned with the layers");
+    static_assert(NMB % 2 == 0, "m-blocks go in pairs");
+    static_assert(H != 512 || NH == 1, "512-wide activations fill the accumulation registers: one hidden layer");
+};
+
+template <int H, int NH, int KS1, int GPS>
+__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPacked pk, int32_t n_tiles) {
+    using G = RGeo<H, NH, KS1>;
+    constexpr int NMB = G::NMB, KS = G::KS, ST = G::ST;
+    extern __shared__ u32x4 smem[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 5;
+    const int col = lane & 31;
+    const int F = in.n_features;
+    // LDS: ring [kNS][16 KB] | X [2][kW][F][64] fp32 | W3 [NMB][2][2][8 rows]
+    // x 16 B + a zero slot | hidden biases [NH][NMB][2][16] fp32
+    char *lds = (char *)smem;
+    const uint32_t lbase = lds_addr(smem);
+    const int xoff = kNS * kStage;
+    const int xbuf_bytes = kW * F * 256;
+    const int xwave = w * F * 256;
+    const int w3off = xoff + 2 * xbuf_bytes;
+    const int zoff = w3off + NMB * 512;
+    const int boff = zoff + 16;
+
+    // the output-layer fragments (rows 0..7) and the hidden biases, staged
+    // once by the block before any direct load is issued
+    {
+        u32x4 *w3l = (u32x4 *)(lds + w3off);
+        const u32x4 *w3g = (const u32x4 *)pk.w3;
+        for (int i = tid; i < NMB * 32; i += kThreads)
+            w3l[i] = w3g[i];
+        if (tid == 0)
+            w3l[NMB * 32] = u32x4{0u, 0u, 0u, 0u};
+        float *bl = (float *)(lds + boff);
+        for (int i = tid; i < NH * NMB * 32; i += kThreads)
+            bl[i] = pk.bias[i];
+    }
+    __syncthreads();
+
+    // input feature table in registers: lane f holds feature f's pointer and
+    // raw offsets; a wave-uniform feature is then three v_readlane_b32
+    const int fl = lane < F ? lane : F - 1;
+    const uint64_t tp = (uint64_t)(uintptr_t)tin.fptr[fl];
+    const uint32_t t_lo = (uint32_t)tp, t_hi = (uint32_t)(tp >> 32), t_raw = tin.raw8[fl];
+    // output table and biases the same way (the from map's outputs share
+    // their raw offsets)
+    const int ol = lane < 8 ? lane : 7;
+    const uint64_t op = (uint64_t)(uintptr_t)tout.fptr[ol];
+    const uint32_t o_lo = (uint32_t)op, o_hi = (uint32_t)(op >> 32);
+    const uint32_t o_b = __builtin_bit_cast(uint32_t, pk.bias_out[ol]);
+    const uint32_t o_raw = tout.raw8[0];
+    const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
+
+    // XCD-aware tile order: blocks on one XCD take adjacent tiles
+    const int nb = gridDim.x;
+    const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
+    if (lb >= n_tiles)
+        return;
+    auto tile_of = [&](int it) { return lb + it * nb; };
+
+    // gather of this wave's 64 points of a tile (lane = point), feature f
+    // into X buffer xb
+    auto gather_point = [&](int tile, Pt32 &pt, uint32_t &edge) {
+        int b = tile * kT + w * kP + lane;
+        b = b < in.n_points ? b : in.n_points - 1;
+        pt = locate32(in, b);
+        edge = edge_dims32(in, pt);
+    };
+    auto gather_one = [&](const Pt32 &pt, uint32_t edge, int f, int xb) {
+        const uint32_t lo = __builtin_amdgcn_readlane(t_lo, f), hi = __builtin_amdgcn_readlane(t_hi, f);
+        const float *base = (const float *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+        int32_t idx = pt.pe;
+        if (edge)
+            idx += edge_fix32(in, pt, __builtin_amdgcn_readlane(t_raw, f), edge);
+        dma4(base + idx, lbase + (uint32_t)(xoff + xb * xbuf_bytes + xwave + f * 256));
+    };
+    // ring stage k (global count) from the tile stream into slot k % kNS
+    const char *wsrc = (const char *)pk.stream + (size_t)(4 * w) * kFrag + (size_t)lane * 16;
+    auto ring_issue = [&](int k) {
+        const int q = k % ST, slot = k % kNS;
+        const char *src = wsrc + (size_t)q * kStage;
+        const uint32_t dst = lbase + (uint32_t)(slot * kStage + 4 * w * kFrag);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            dma16(src + i * kFrag, dst + i * kFrag);
+    };
+
+    // ---- prologue: the first two tiles' inputs, the first kD stages
+    {
+        Pt32 pt;
+        uint32_t edge;
+        for (int i = 0; i < 2; ++i) {
+            const int tt = tile_of(i) < n_tiles ? tile_of(i) : n_tiles - 1;
+            gather_point(tt, pt, edge);
+            for (int f = 0; f < F; ++f)
+                gather_one(pt, edge, f, i);
+        }
+        for (int k = 0; k < kD; ++k)
+            ring_issue(k);
+        vm_wait<0>();
+        block_barrier();
+    }
+
+    Pt32 gpt;                        // gather point of tile it + 2
+    uint32_t gedge = 0;
+    int gx = 0;                      // its X buffer
+    int kb = 0;                      // global stage index of this tile's first stage
+    const u32x4 *fr_lane = smem + lane;
+
+    // publication of stage s + 1 of this tile (at fragment kSync of stage s):
+    // this wave's loads of it have landed, then every wave's; then the next
+    // loads go out (stage s + kD reuses the slot of stage s - 1, which every
+    // wave finished before the barrier)
+    auto sync = [&](int s) {
+        vm_wait<(kD - 2) * (GPS + 4)>();
+        block_barrier();
+#pragma unroll
+        for (int i = 0; i < GPS; ++i) {
+            const int f = s * GPS + i;
+            gather_one(gpt, gedge, f < F ? f : F - 1, gx);
+        }
+        ring_issue(kb + s + kD);
+    };
+    // the fragment pipeline: the read of the fragment at stream position
+    // p + kPd is issued at position p (PC compile-time, pr a runtime multiple
+    // of kSF), after publishing the next stage when p + kPd enters it
+    u32x4 a[kR];
+    auto frag_ptr = [&](int p) { return fr_lane + ((kb + p / kSF) % kNS) * (kStage / 16) + (p % kSF) * (kFrag / 16); };
+    auto fragment = [&](auto PC, int pr) -> bf16x8 {
+        constexpr int pc = decltype(PC)::value;
+        if constexpr (pc % kSF == kSync)
+            sync((pc + pr) / kSF);
+        a[(pc + kPd) % kR] = *frag_ptr(pc + pr + kPd);
+        return as_bf16x8(a[pc % kR]);
+    };
+    // K loop of one m-block: fragments at positions PC0 + pr + s, B operands
+    // hin[s], accumulators (c0, c1) from zero; mid(S) runs after K-step S
+    // (the previous m-block's epilogue, spread over the loop)
+    auto kloop = [&](auto PC0, int pr, auto NK, const u32x4 (*hin)[2], floatx16 &c0, floatx16 &c1, auto mid) {
+        static_for<0, decltype(NK)::value>([&](auto S) {
+            constexpr int s = decltype(S)::value;
+            const bf16x8 av = fragment(std::integral_constant<int, decltype(PC0)::value + s>{}, pr);
+            const floatx16 zero = {};
+            c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][0]), s == 0 ? zero : c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][1]), s == 0 ? zero : c1, 0, 0, 0);
+            mid(S);
+        });
+    };
+    // biases of hidden layer l, m-block j, in the accumulator layout
+    auto bias_of = [&](int l, int j) -> floatx16 {
+        const floatx4 *bp = (const floatx4 *)(lds + boff + ((l * NMB + j) * 2 + g) * 64);
+        floatx16 b;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const floatx4 v = bp[q];
+            b[4 * q + 0] = v[0];
+            b[4 * q + 1] = v[1];
+            b[4 * q + 2] = v[2];
+            b[4 * q + 3] = v[3];
+        }
+        return b;
+    };
+    // output-layer fragment t of m-block j (rows >= 8 read the zero slot)
+    const int w3lane = (g * 8 + (col & 7)) * 16;
+    auto wo_of = [&](int j, int t) -> bf16x8 {
+        const int off = col < 8 ? w3off + (2 * j + t) * 256 + w3lane : zoff;
+        return as_bf16x8(*(const u32x4 *)(lds + off));
+    };
+
+#pragma unroll
+    for (int p = 0; p < kPd; ++p)
+        a[p] = *frag_ptr(p);
+
+    u32x4 h[NH > 1 ? 2 : 1][KS][2];  // activations: B fragments [K-step][n-block]
+    floatx16 acc[2][2];
+
+    for (int it = 0; tile_of(it) < n_tiles; ++it) {
+        const int tile = tile_of(it);
+        {
+            int tg = tile_of(it + 2);
+            tg = tg < n_tiles ? tg : n_tiles - 1;
+            gather_point(tg, gpt, gedge);
+            gx = it & 1;
+        }
+
+        // ---- this tile's inputs (X buffer it & 1) as layer-1 B fragments;
+        //      features F..F+2 carry the first-layer bias
+        u32x4 xb[KS1][2];
+        {
+            const float *xa = (const float *)(lds + xoff + (it & 1) * xbuf_bytes + xwave);
+#pragma unroll
+            for (int s = 0; s < KS1; ++s)
+#pragma unroll
+                for (int n = 0; n < 2; ++n) {
+                    float v[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const int f = 16 * s + 8 * g + e;
+                        const int fc = f < F ? f : F - 1;
+                        const float x = xa[fc * 64 + 32 * n + col];
+                        v[e] = f < F ? x : (f < F + 3 ? 1.f : 0.f);
+                    }
+                    xb[s][n] = u32x4{pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])};
+                }
+        }
+
+        // ---- layer 1, m-block by m-block; the epilogue of m-block j - 1
+        //      (activation, bf16 -> K-steps 2j - 2, 2j - 1 of the next layer)
+        //      after the first K-step of m-block j
+        {
+            auto epi1 = [&](auto J) {
+                constexpr int j = decltype(J)::value;
+                static_for<0, 2>([&](auto T) {
+                    constexpr int t = decltype(T)::value;
+                    h[0][2 * j + t][0] = to_agpr(to_b(acc[j & 1][0], t));
+                    h[0][2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t));
+                });
+            };
+            static_for<0, NMB>([&](auto J) {
+                constexpr int j = decltype(J)::value;
+                kloop(std::integral_constant<int, j * KS1>{}, 0, std::integral_constant<int, KS1>{}, xb,
+                      acc[j & 1][0], acc[j & 1][1], [&](auto S) {
+                          if constexpr (decltype(S)::value == 0 && j > 0)
+                              epi1(std::integral_constant<int, j - 1>{});
+                      });
+            });
+            // the first layer's padding fragments (its stages are whole)
+            static_for<G::L1F, G::L1S * kSF>([&](auto P) { (void)fragment(P, 0); });
+            epi1(std::integral_constant<int, NMB - 1>{});
+        }
+
+        // ---- hidden layers before the last: m-blocks unrolled (their
+        //      activations land in statically indexed registers)
+        static_for<0, NH - 1>([&](auto L) {
+            constexpr int l = decltype(L)::value;
+            const u32x4(*hin)[2] = h[l % 2];
+            u32x4(*hout)[2] = h[(l + 1) % 2];
+            auto epih = [&](auto J) {
+                constexpr int j = decltype(J)::value;
+                const floatx16 bias = bias_of(l, j);
+                static_for<0, 2>([&](auto T) {
+                    constexpr int t = decltype(T)::value;
+                    hout[2 * j + t][0] = to_agpr(to_b(acc[j & 1][0], t, bias));
+                    hout[2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t, bias));
+                });
+            };
+            static_for<0, NMB>([&](auto J) {
+                constexpr int j = decltype(J)::value;
+                kloop(std::integral_constant<int, G::L1S * kSF + l * G::HF + j * KS>{}, 0,
+                      std::integral_constant<int, KS>{}, hin, acc[j & 1][0], acc[j & 1][1], [&](auto S) {
+                          if constexpr (decltype(S)::value == 1 && j > 0)
+                              epih(std::integral_constant<int, j - 1>{});
+                      });
+            });
+            epih(std::integral_constant<int, NMB - 1>{});
+        });
+
+        // ---- last hidden layer, streamed into the output layer: m-blocks in
+        //      a loop of pairs; the epilogue of one (bias, activation, bf16,
+        //      its share of the output layer) is spread over the next one's
+        //      first K-steps
+        {
+            constexpr int l = NH - 1;
+            const u32x4(*hin)[2] = h[l % 2];
+            using P0 = std::integral_constant<int, G::L1S * kSF + l * G::HF>;   // stream position of the layer
+            using NKS = std::integral_constant<int, KS>;
+            floatx16 y0 = {}, y1 = {};
+            // part q of the epilogue of m-block j (accumulators c): K-step
+            // t = q / 2 of the output layer for n-block q % 2
+            auto epi_part = [&](auto Q, int j, floatx16 (&c)[2]) {
+                constexpr int q = decltype(Q)::value, t = q >> 1;
+                const floatx16 bias = bias_of(l, j);
+                const bf16x8 wo = wo_of(j, t);
+                if constexpr (q & 1) {
+                    const u32x4 b1 = to_b(c[1], t, bias);
+                    y1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wo, as_bf16x8(b1), y1, 0, 0, 0);
+                } else {
+                    const u32x4 b0 = to_b(c[0], t, bias);
+                    y0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wo, as_bf16x8(b0), y0, 0, 0, 0);
+                }
+            };
+            // m-block j into accumulators cur; the epilogue of m-block j - 1
+            // (accumulators prev) at K-steps 1, 3, 5, 7
+            auto mblock = [&](int j, floatx16 (&cur)[2], floatx16 (&prev)[2], bool first) {
+                kloop(P0{}, j * KS, NKS{}, hin, cur[0], cur[1], [&](auto S) {
+                    constexpr int s = decltype(S)::value;
+                    if constexpr (s == 1 || s == 3 || s == 5 || s == 7) {
+                        if (!first)
+                            epi_part(std::integral_constant<int, (s >> 1)>{}, j - 1, prev);
+                    }
+                });
+            };
+            mblock(0, acc[0], acc[1], true);
+            for (int j = 1; j < NMB - 1; j += 2) {
+                mblock(j, acc[1], acc[0], false);
+                mblock(j + 1, acc[0], acc[1], false);
+            }
+            mblock(NMB - 1, acc[1], acc[0], false);
+            static_for<0, 4>([&](auto Q) { epi_part(Q, NMB - 1, acc[1]); });
+
+            // ---- scatter: y rows are outputs (row 4 g + r in register r < 4),
+            //      lanes are points
+#pragma unroll
+            for (int n = 0; n < 2; ++n) {
+                const floatx16 &y = n ? y1 : y0;
+                const int b = tile * kT + w * kP + 32 * n + col;
+                const Pt32 pt = locate32(out, b < out.n_points ? b : out.n_points - 1);
+                const uint32_t edge = edge_dims32(out, pt);
+                int32_t idx = pt.pe;
+                if (edge)
+                    idx += edge_fix32(out, pt, o_raw, edge);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int o = r + 4 * g;
+                    if (o < pk.f_out && b < out.n_points) {
+                        const uint32_t lo0 = __builtin_amdgcn_readlane(o_lo, r), lo1 = __builtin_amdgcn_readlane(o_lo, r + 4);
+                        const uint32_t hi0 = __builtin_amdgcn_readlane(o_hi, r), hi1 = __builtin_amdgcn_readlane(o_hi, r + 4);
+                        const float bo0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(o_b, r));
+                        const float bo1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(o_b, r + 4));
+                        float v = y[r] + (g ? bo1 : bo0);
+                        if (orelu)
+                            v = fmaxf(v, 0.f);
+                        float *dst = (float *)(uintptr_t)(((uint64_t)(g ? hi1 : hi0) << 32) | (g ? lo1 : lo0));
+                        stg(dst + idx, v);
+                    }
+                }
+            }
+        }
+        kb += ST;
+    }
+    // every direct load has landed before the block's LDS is released
+    vm_wait<0>();
+}
+
+// feature of the previous layer's output held at element e (lane half g) of
+// K-step s of a B fragment built from C registers 8 (s % 2) .. + 7 of m-block
+// s / 2
+int b_feature(int s, int g, int e) { return 32 * (s / 2) + 16 * (s % 2) + 8 * (e / 4) + 4 * g + e % 4; }
+
+int ring_stages(int H, int n_hidden, int ks1) {
+    const int l1f = (H / 32) * ks1;
+    return (l1f + kSF - 1) / kSF + n_hidden * (H / 32) * (H / 16) / kSF;
+}
+
+// first-layer K-steps and gathers per ring stage of a shape
+int bf16r_ks1(int f_in) { return (f_in + 3 + 15) / 16; }
+int bf16r_gps(int H, int n_hidden, int f_in) {
+    const int st = ring_stages(H, n_hidden, bf16r_ks1(f_in));
+    return (f_in + st - 1) / st;
+}
+
+// LDS of one block: ring, two input buffers, output fragments (+ a zero
+// slot), hidden biases
+size_t bf16r_lds_bytes(int H, int n_hidden, int f_in) {
+    return (size_t)kNS * kStage + (size_t)2 * kW * f_in * 256 + (size_t)(H / 32) * 512 + 16 +
+           (size_t)n_hidden * (H / 32) * 128;
+}
+
+template <int H, int NH, int KS1, int GPS>
+hipError_t launch_r(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                    const BF16RPacked &pk, hipStream_t stream) {
+    const int32_t n_tiles = (in.n_points + kT - 1) / kT;
+    const size_t lds = bf16r_lds_bytes(H, NH, in.n_features);
+    int dev = 0, cus = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int32_t grid = n_tiles < cus ? n_tiles : cus;
+    auto kern = mlp_bf16r_kernel<H, NH, KS1, GPS>;
+    hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(kThreads), lds, stream, in, out, tin, tout, pk, n_tiles);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool bf16r_supported(int n_layers, const int32_t *dims, const int32_t *act, int compute) {
+    if (compute != HPACML_BF16 || n_layers < 3)
+        return false;
+    const int H = dims[1], nh = n_layers - 2;
+    if (!((H == 512 && nh == 1) || (H == 256 && nh <= 2)))
+        return false;
+    for (int l = 1; l < n_layers; ++l)
+        if (dims[l] != H)
+            return false;
+    for (int l = 0; l + 1 < n_layers; ++l)
+        if (act[l] != HPACML_ACT_RELU)
+            return false;
+    const int f_in = dims[0], ks1 = bf16r_ks1(f_in);
+    if (dims[n_layers] > 8)
+        return false;
+    // instantiated shapes
+    if (!((H == 512 && ks1 == 3) || (H == 256 && nh == 2 && ks1 == 1)))
+        return false;
+    if (bf16r_lds_bytes(H, nh, f_in) > 160 * 1024)
+        return false;
+    return bf16r_gps(H, nh, f_in) <= 2;
+}
+
+// Stream of one tile: the first layer's fragments (m-block j, K-step s at
+// position j * ks1 + s; column F..F+2 = the bias split in three bf16 terms),
+// padded to whole stages, then each hidden layer's (m-block j, K-step s at
+// j * H/16 + s, columns permuted to the B-fragment order).  A fragment is
+// lane l = (i = l % 32, g = l / 32) x 8 elements: A[i][8 g + e].
+void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
+                std::vector<uint8_t> &buf, size_t *off_w3, size_t *off_bias, BF16RPacked *pk) {
+    const int H = dims[1], F = dims[0], Fo = dims[n_layers];
+    const int NMB = H / 32, KS = H / 16, nh = n_layers - 2;
+    const int ks1 = bf16r_ks1(F);
+    const int st = ring_stages(H, nh, ks1);
+    const int l1s = (NMB * ks1 + kSF - 1) / kSF;
+    std::vector<uint16_t> stream((size_t)st * kSF * 64 * 8, 0);
+    auto put = [&](int pos, int l, int e, uint16_t v) { stream[((size_t)pos * 64 + l) * 8 + e] = v; };
+    for (int j = 0; j < NMB; ++j)
+        for (int s = 0; s < ks1; ++s)
+            for (int l = 0; l < 64; ++l)
+                for (int e = 0; e < 8; ++e) {
+                    const int o = 32 * j + l % 32, k = 16 * s + 8 * (l / 32) + e;
+                    uint16_t v = 0;
+                    if (k < F) {
+                        v = bf16_rne_host(W[0][(size_t)o * F + k]);
+                    } else if (k < F + 3) {
+                        uint16_t t[3];
+                        split_bias(b[0][o], t);
+                        v = t[k - F];
+                    }
+                    put(j * ks1 + s, l, e, v);
+                }
+    for (int h = 0; h < nh; ++h)
+        for (int j = 0; j < NMB; ++j)
+            for (int s = 0; s < KS; ++s)
+                for (int l = 0; l < 64; ++l)
+                    for (int e = 0; e < 8; ++e) {
+                        const int o = 32 * j + l % 32;
+                        const int k = b_feature(s, l / 32, e);
+                        put(l1s * kSF + (h * NMB + j) * KS + s, l, e, bf16_rne_host(W[h + 1][(size_t)o * H + k]));
+                    }
+    // output layer: m-block j, K-step t, lane half g, row i < 8 (16 bytes each)
+    std::vector<uint16_t> w3((size_t)NMB * 2 * 2 * 8 * 8, 0);
+    for (int j = 0; j < NMB; ++j)
+        for (int t = 0; t < 2; ++t)
+            for (int g = 0; g < 2; ++g)
+                for (int i = 0; i < 8; ++i)
+                    for (int e = 0; e < 8; ++e) {
+                        const int k = b_feature(2 * j + t, g, e);
+                        w3[((((size_t)j * 2 + t) * 2 + g) * 8 + i) * 8 + e] =
+                            i < Fo ? bf16_rne_host(W[n_layers - 1][(size_t)i * H + k]) : 0;
+                    }
+    std::vector<float> bias((size_t)nh * NMB * 2 * 16);
+    for (int h = 0; h < nh; ++h)
+        for (int j = 0; j < NMB; ++j)
+            for (int g = 0; g < 2; ++g)
+                for (int r = 0; r < 16; ++r)
+                    bias[(((size_t)h * NMB + j) * 2 + g) * 16 + r] = b[h + 1][32 * j + 8 * (r / 4) + 4 * g + r % 4];
+    buf.assign(stream.size() * 2 + w3.size() * 2 + bias.size() * 4, 0);
+    std::memcpy(buf.data(), stream.data(), stream.size() * 2);
+    *off_w3 = stream.size() * 2;
+    std::memcpy(buf.data() + *off_w3, w3.data(), w3.size() * 2);
+    *off_bias = *off_w3 + w3.size() * 2;
+    std::memcpy(buf.data() + *off_bias, bias.data(), bias.size() * 4);
+    pk->hid = H;
+    pk->n_hidden = nh;
+    pk->ks1 = ks1;
+    pk->f_out = Fo;
+    pk->stages = st;
+    for (int i = 0; i < 16; ++i)
+        pk->bias_out[i] = i < Fo ? b[n_layers - 1][i] : 0.f;
+}
+
+hipError_t launch_mlp_bf16r(const Map32 &in, const Map32 &out, const FeatTable32 &tin, const FeatTable32 &tout,
+                            const BF16RPacked &pk, hipStream_t stream) {
+    if (in.n_points == 0)
+        return hipSuccess;
+    const int gps = bf16r_gps(pk.hid, pk.n_hidden, in.n_features);
+#define HPACML_R(H, NH, KS1)                                                                  \
+    if (pk.hid == H && pk.n_hidden == NH && pk.ks1 == KS1)                                    \
+        return gps == 1 ? launch_r<H, NH, KS1, 1>(in, out, tin, tout, pk, stream)         \
+                        : launch_r<H, NH, KS1, 2>(in, out, tin, tout, pk, stream);
+    HPACML_R(512, 1, 3)
+    HPACML_R(256, 2, 1)
+#undef HPACML_R
+    return hipErrorInvalidValue;
+}
+
+const char *bf16r_variant_name(const BF16RPacked &pk) {
+    return pk.hid == 512 ? "mlp_bf16r_h512" : "mlp_bf16r_h256";
+}
+
+}  // namespace hpacml

@@ -185,7 +185,7 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatT
             for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    acc[mb][r] = relu_arith(acc[mb][r]);
+                    acc[mb][r] = relu_mfma(acc[mb][r]);
         }
 
         // ---- hidden layers H -> H
@@ -209,7 +209,7 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatT
                 for (int mb = 0; mb < NMB; ++mb)
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
-                        acc[mb][r] = relu_arith(acc[mb][r]);
+                        acc[mb][r] = relu_mfma(acc[mb][r]);
             }
         }
 

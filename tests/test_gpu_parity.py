@@ -283,12 +283,12 @@ def test_infer_nan_inputs_follow_relu(name):
 
 @pytest.mark.parametrize("shape", [(9, 5, 256), (3, 2, 128)])
 def test_stencil3d_plane_order_visit(shape):
-    """Rows made of whole 128-point tiles: the bf16 kernel visits tiles with
-    the plane index fastest; every cell must still be written exactly as the
-    oracle's region writes it."""
+    """Rows made of whole tiles (128 points of the LDS-resident bf16 kernel,
+    256 of the register-resident one); every cell must be written exactly as
+    the oracle's region writes it."""
     w = wl.make("stencil3d", shape)
     got, var = run_infer(w)
-    assert var.startswith("mlp_bf16_h512"), var
+    assert var.startswith("mlp_bf16r_h512"), var
     Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
     exp = [o.copy() for o in w.outputs]
     oracle.scatter(w.out_spec, exp, Y)
@@ -300,7 +300,7 @@ def test_stencil3d_plane_order_visit(shape):
 
 def test_infer_fast_paths_are_used():
     for name, want in [("options", "mlp_f32_h64"), ("bonds", "mlp_f32_h128"), ("stencil2d", "mlp_f32_h128"),
-                       ("poses", "mlp_bf16_h256"), ("stencil3d", "mlp_bf16_h512")]:
+                       ("poses", "mlp_bf16r_h256"), ("stencil3d", "mlp_bf16r_h512")]:
         w = wl.make(name, {"stencil2d": (20, 40), "stencil3d": (6, 7, 9)}.get(name, 1000))
         _, var = run_infer(w)
         assert var.startswith(want), (name, var)
@@ -311,7 +311,9 @@ def test_infer_fast_paths_are_used():
     ("f32", 64, 57, 8, "mlp_f32_h64_k64"), ("f32", 128, 16, 2, "mlp_f32_h128_k16"),
     ("f32", 128, 40, 4, "mlp_f32_h128_k40"), ("f32", 128, 64, 1, "mlp_f32_h128_k64"),
     ("bf16", 256, 13, 16, "mlp_bf16_h256"), ("bf16", 512, 7, 2, "mlp_bf16_h512"),
-    ("bf16", 512, 45, 5, "mlp_bf16_h512"), ("bf16", 512, 61, 9, "mlp_bf16_h512")])
+    ("bf16", 512, 45, 5, "mlp_bf16_h512"), ("bf16", 512, 61, 9, "mlp_bf16_h512"),
+    ("bf16", 512, 35, 5, "mlp_bf16r_h512"), ("bf16", 512, 30, 8, "mlp_bf16r_h512"),
+    ("bf16", 512, 42, 1, "mlp_bf16r_h512")])
 def test_fast_kernels_input_widths(compute, H, F_in, F_out, want):
     """Every template variant of the MFMA kernels (input width classes,
     widths of hidden layers, output counts), pointwise maps with a ragged
