@@ -36,6 +36,8 @@
 // slot from another); their completion is this kernel's own count of
 // vector-memory loads, and the barriers that publish their data are
 // assembly with a memory clobber, so no LDS access moves across one.
+#include <cfloat>
+#include <cstddef>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -72,22 +74,22 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
-// registers 8t..8t+7 of a C fragment, plus the bias, after ReLU (max(x, 0),
-// a NaN giving 0), as a B fragment of the next layer.  Plain fmaxf, so the
-// compiler sees the vector ALU reading the MFMA's result and keeps the wait
-// states that read requires.
-__device__ __forceinline__ u32x4 to_b(const floatx16 &c, int t, const floatx16 &bias) {
-    float v[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e)
-        v[e] = __builtin_fmaxf(c[8 * t + e] + bias[8 * t + e], 0.f);
-    return u32x4{pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])};
-}
+// ReLU of an MFMA result that is rounded to bf16 next: one v_med3_f32(x, 0,
+// FLT_MAX), which the compiler sees (so it keeps the wait states a vector
+// ALU read of an MFMA result needs).  A NaN gives 0 (v_med3_f32 returns the
+// minimum of the non-NaN operands then); +inf gives FLT_MAX, which rounds to
+// bf16 +inf, so the bf16 result is that of max(x, 0) in every case.  (With an
+// upper bound of +inf the compiler rewrites it as a maximum and quiets x
+// first: two instructions.)
+__device__ __forceinline__ float relu_to_bf16(float x) { return __builtin_amdgcn_fmed3f(x, 0.f, FLT_MAX); }
+
+// registers 8t..8t+7 of a C fragment after ReLU, as a B fragment of the next
+// layer (the bias is in the accumulator already)
 __device__ __forceinline__ u32x4 to_b(const floatx16 &c, int t) {
     float v[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e)
-        v[e] = relu_mfma(c[8 * t + e]);
+        v[e] = relu_to_bf16(c[8 * t + e]);
     return u32x4{pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])};
 }
 
@@ -127,6 +129,73 @@ __device__ __forceinline__ void dma4(const void *g, uint32_t lds) {
 
 __device__ __forceinline__ uint32_t lds_addr(const void *p) {
     return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// A map in one vector register: lane i holds 32-bit word i of its Map32, and
+// a field is one v_readlane_b32 where it is used.  (Held by value, the maps'
+// fields would sit in scalar registers for the whole kernel and spill.)
+// `fresh()` hides the register's value from the compiler, so readings after
+// it are made again rather than kept live from before.  Every dimension is
+// resolved without branching on the rank: a map's unused dimensions have
+// count 1, start 0, stride 0, extent 1 and no offsets, so they add nothing.
+constexpr int kMapWords = (int)(sizeof(Map32) / 4);
+static_assert(kMapWords <= 64, "one word per lane");
+#define HPACML_MW(field) ((int)(offsetof(Map32, field) / 4))
+struct LaneMap {
+    int32_t v;
+    __device__ void load(const Map32 &m, int lane) { v = ((const int32_t *)&m)[lane < kMapWords ? lane : 0]; }
+    __device__ void fresh() { asm volatile("" : "+v"(v)); }
+    __device__ int32_t word(int i) const { return __builtin_amdgcn_readlane(v, i); }
+};
+
+__device__ __forceinline__ Pt32 locate_lm(const LaneMap &m, int32_t b) {
+    Pt32 r;
+    uint32_t rem = (uint32_t)b;
+    r.pe = 0;
+#pragma unroll
+    for (int d = HPACML_MAX_RANK - 1; d >= 0; --d) {
+        const uint32_t magic = (uint32_t)m.word(HPACML_MW(magic) + d);
+        const int32_t shift = m.word(HPACML_MW(shift) + d);
+        const uint32_t q = (uint32_t)(((uint64_t)rem * magic) >> shift);
+        const int32_t k = (int32_t)(rem - q * (uint32_t)m.word(HPACML_MW(count) + d));
+        rem = q;
+        const int32_t x = m.word(HPACML_MW(start) + d) + k * m.word(HPACML_MW(step) + d);
+        r.p[d] = x;
+        r.pe += x * m.word(HPACML_MW(stride) + d);
+    }
+    return r;
+}
+
+// dimensions along which some lane's window leaves the arrays (wave-uniform)
+__device__ __forceinline__ uint32_t edge_dims_lm(const LaneMap &m, const Pt32 &r) {
+    uint32_t edge = 0;
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d)
+        if (__any(r.p[d] + m.word(HPACML_MW(omin) + d) < 0 ||
+                  r.p[d] + m.word(HPACML_MW(omax) + d) >= m.word(HPACML_MW(extent) + d)))
+            edge |= 1u << d;
+    return edge;
+}
+
+// boundary correction of a feature with raw offsets raw8 (signed bytes) at
+// point r along the dimensions in `edge`: periodic wraps once, clamp
+// saturates; added to the interior element index
+__device__ __forceinline__ int32_t edge_fix_lm(const LaneMap &m, const Pt32 &r, uint32_t raw8, uint32_t edge) {
+    int32_t fix = 0;
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        if (edge & (1u << d)) {
+            const int32_t q = r.p[d] + (int32_t)(int8_t)(raw8 >> (8 * d));
+            const int32_t n = m.word(HPACML_MW(extent) + d);
+            int32_t c;
+            if (m.word(HPACML_MW(bnd) + d) == HPACML_BND_PERIODIC)
+                c = (n & (q >> 31)) - (n & ~((q - n) >> 31));
+            else
+                c = max(0, min(q, n - 1)) - q;
+            fix += c * m.word(HPACML_MW(stride) + d);
+        }
+    }
+    return fix;
 }
 
 // compile-time loop: fn(std::integral_constant<int, i>) for i in [B, E)
@@ -204,6 +273,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
     const uint32_t o_b = __builtin_bit_cast(uint32_t, pk.bias_out[ol]);
     const uint32_t o_raw = tout.raw8[0];
     const bool orelu = pk.act[pk.n_hidden + 1] == HPACML_ACT_RELU;
+    LaneMap lin, lout;
+    lin.load(in, lane);
+    lout.load(out, lane);
 
     // XCD-aware tile order: blocks on one XCD take adjacent tiles
     const int nb = gridDim.x;
@@ -217,15 +289,18 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
     auto gather_point = [&](int tile, Pt32 &pt, uint32_t &edge) {
         int b = tile * kT + w * kP + lane;
         b = b < in.n_points ? b : in.n_points - 1;
-        pt = locate32(in, b);
-        edge = edge_dims32(in, pt);
+        lin.fresh();
+        pt = locate_lm(lin, b);
+        edge = edge_dims_lm(lin, pt);
     };
     auto gather_one = [&](const Pt32 &pt, uint32_t edge, int f, int xb) {
         const uint32_t lo = __builtin_amdgcn_readlane(t_lo, f), hi = __builtin_amdgcn_readlane(t_hi, f);
         const float *base = (const float *)(uintptr_t)(((uint64_t)hi << 32) | lo);
         int32_t idx = pt.pe;
-        if (edge)
-            idx += edge_fix32(in, pt, __builtin_amdgcn_readlane(t_raw, f), edge);
+        if (edge) {
+            lin.fresh();
+            idx += edge_fix_lm(lin, pt, __builtin_amdgcn_readlane(t_raw, f), edge);
+        }
         dma4(base + idx, lbase + (uint32_t)(xoff + xb * xbuf_bytes + xwave + f * 256));
     };
     // ring stage k (global count) from the tile stream into slot k % kNS
@@ -288,15 +363,16 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
         return as_bf16x8(a[pc % kR]);
     };
     // K loop of one m-block: fragments at positions PC0 + pr + s, B operands
-    // hin[s], accumulators (c0, c1) from zero; mid(S) runs after K-step S
-    // (the previous m-block's epilogue, spread over the loop)
-    auto kloop = [&](auto PC0, int pr, auto NK, const u32x4 (*hin)[2], floatx16 &c0, floatx16 &c1, auto mid) {
+    // hin[s], accumulators (c0, c1) from cinit (zero, or the layer's biases);
+    // mid(S) runs after K-step S (the previous m-block's epilogue, spread
+    // over the loop)
+    auto kloop = [&](auto PC0, int pr, auto NK, const u32x4 (*hin)[2], floatx16 &c0, floatx16 &c1,
+                     const floatx16 &cinit, auto mid) {
         static_for<0, decltype(NK)::value>([&](auto S) {
             constexpr int s = decltype(S)::value;
             const bf16x8 av = fragment(std::integral_constant<int, decltype(PC0)::value + s>{}, pr);
-            const floatx16 zero = {};
-            c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][0]), s == 0 ? zero : c0, 0, 0, 0);
-            c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][1]), s == 0 ? zero : c1, 0, 0, 0);
+            c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][0]), s == 0 ? cinit : c0, 0, 0, 0);
+            c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][1]), s == 0 ? cinit : c1, 0, 0, 0);
             mid(S);
         });
     };
@@ -370,12 +446,13 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                     h[0][2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t));
                 });
             };
+            const floatx16 zero = {};
             static_for<0, NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
                 kloop(std::integral_constant<int, j * KS1>{}, 0, std::integral_constant<int, KS1>{}, xb,
-                      acc[j & 1][0], acc[j & 1][1], [&](auto S) {
+                      acc[j & 1][0], acc[j & 1][1], zero, [&](auto S) {
                           if constexpr (decltype(S)::value == 0 && j > 0)
-                              epi1(std::integral_constant<int, j - 1>{});
+                              epi1(std::integral_constant<int, (j > 0 ? j - 1 : 0)>{});
                       });
             });
             // the first layer's padding fragments (its stages are whole)
@@ -391,19 +468,19 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             u32x4(*hout)[2] = h[(l + 1) % 2];
             auto epih = [&](auto J) {
                 constexpr int j = decltype(J)::value;
-                const floatx16 bias = bias_of(l, j);
                 static_for<0, 2>([&](auto T) {
                     constexpr int t = decltype(T)::value;
-                    hout[2 * j + t][0] = to_agpr(to_b(acc[j & 1][0], t, bias));
-                    hout[2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t, bias));
+                    hout[2 * j + t][0] = to_agpr(to_b(acc[j & 1][0], t));
+                    hout[2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t));
                 });
             };
             static_for<0, NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
                 kloop(std::integral_constant<int, G::L1S * kSF + l * G::HF + j * KS>{}, 0,
-                      std::integral_constant<int, KS>{}, hin, acc[j & 1][0], acc[j & 1][1], [&](auto S) {
+                      std::integral_constant<int, KS>{}, hin, acc[j & 1][0], acc[j & 1][1], bias_of(l, j),
+                      [&](auto S) {
                           if constexpr (decltype(S)::value == 1 && j > 0)
-                              epih(std::integral_constant<int, j - 1>{});
+                              epih(std::integral_constant<int, (j > 0 ? j - 1 : 0)>{});
                       });
             });
             epih(std::integral_constant<int, NMB - 1>{});
@@ -423,20 +500,19 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             // t = q / 2 of the output layer for n-block q % 2
             auto epi_part = [&](auto Q, int j, floatx16 (&c)[2]) {
                 constexpr int q = decltype(Q)::value, t = q >> 1;
-                const floatx16 bias = bias_of(l, j);
                 const bf16x8 wo = wo_of(j, t);
                 if constexpr (q & 1) {
-                    const u32x4 b1 = to_b(c[1], t, bias);
+                    const u32x4 b1 = to_b(c[1], t);
                     y1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wo, as_bf16x8(b1), y1, 0, 0, 0);
                 } else {
-                    const u32x4 b0 = to_b(c[0], t, bias);
+                    const u32x4 b0 = to_b(c[0], t);
                     y0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wo, as_bf16x8(b0), y0, 0, 0, 0);
                 }
             };
             // m-block j into accumulators cur; the epilogue of m-block j - 1
             // (accumulators prev) at K-steps 1, 3, 5, 7
             auto mblock = [&](int j, floatx16 (&cur)[2], floatx16 (&prev)[2], bool first) {
-                kloop(P0{}, j * KS, NKS{}, hin, cur[0], cur[1], [&](auto S) {
+                kloop(P0{}, j * KS, NKS{}, hin, cur[0], cur[1], bias_of(l, j), [&](auto S) {
                     constexpr int s = decltype(S)::value;
                     if constexpr (s == 1 || s == 3 || s == 5 || s == 7) {
                         if (!first)
@@ -458,11 +534,12 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             for (int n = 0; n < 2; ++n) {
                 const floatx16 &y = n ? y1 : y0;
                 const int b = tile * kT + w * kP + 32 * n + col;
-                const Pt32 pt = locate32(out, b < out.n_points ? b : out.n_points - 1);
-                const uint32_t edge = edge_dims32(out, pt);
+                lout.fresh();
+                const Pt32 pt = locate_lm(lout, b < out.n_points ? b : out.n_points - 1);
+                const uint32_t edge = edge_dims_lm(lout, pt);
                 int32_t idx = pt.pe;
                 if (edge)
-                    idx += edge_fix32(out, pt, o_raw, edge);
+                    idx += edge_fix_lm(lout, pt, o_raw, edge);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int o = r + 4 * g;
