@@ -62,6 +62,7 @@ DESCRIPTION = {
 KERNEL_SOURCES = {
     "collect": ["collect.hip", "device.hpp", "kernels.hpp"],
     "mlp_f32": ["mlp_f32.hip", "device.hpp", "kernels.hpp"],
+    "mlp_bf16r": ["mlp_bf16r.hip", "device.hpp", "kernels.hpp"],
     "mlp_bf16": ["mlp_bf16.hip", "device.hpp", "kernels.hpp"],
     "mlp_generic": ["mlp_generic.hip", "device.hpp", "kernels.hpp"],
     "cnn_": ["cnn.hip", "cnn.hpp", "device.hpp", "kernels.hpp"],

@@ -62,9 +62,17 @@ constexpr int kSF = 16;                // fragments per ring stage
 constexpr int kStage = kSF * kFrag;    // 16 KB
 constexpr int kPd = 4;                 // fragment reads in flight ahead of their use
 constexpr int kR = 8;                  // fragments held in registers (> kPd, divides the layers' fragment counts)
-constexpr int kSync = kSF - kPd;       // fragment of a stage at which the next one is published
+constexpr int kSync = kSF - kPd - 2;   // fragment of a stage at which the next one is published
+// after it, one direct load of the next ring stage per fragment, then the
+// stage's gathers: the memory work of a stage goes out between matrix
+// instructions instead of in one block after the barrier
+static_assert(kSync + 5 < kSF, "four ring loads and the gathers fit after the barrier");
 constexpr int kNS = 4;                 // ring stages in LDS
 constexpr int kD = kNS - 1;            // stages loaded ahead
+// scheduling-barrier mask: only VALU, SALU and transcendental instructions
+// may be moved across (the matrix instructions and memory accesses keep
+// their order)
+constexpr int kSchedAluOnly = 0x2 | 0x4 | 0x400;
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
@@ -166,34 +174,57 @@ __device__ __forceinline__ Pt32 locate_lm(const LaneMap &m, int32_t b) {
     return r;
 }
 
-// dimensions along which some lane's window leaves the arrays (wave-uniform)
-__device__ __forceinline__ uint32_t edge_dims_lm(const LaneMap &m, const Pt32 &r) {
-    uint32_t edge = 0;
+// A gather point: the element index of a sweep point and, per dimension,
+// the smallest and largest offset that stay inside the arrays (-coordinate
+// and extent - 1 - coordinate); unused dimensions give 0 and 0.
+struct GPt {
+    int32_t pe;
+    int32_t lo[HPACML_MAX_RANK], hi[HPACML_MAX_RANK];
+};
+
+// Boundary correction of a windowed access (raw offsets raw8, signed bytes,
+// wave-uniform) at gather point r: per dimension dl = clamp(offset, lo, hi)
+// - offset (zero inside); clamp adds dl strides, periodic adds sign(dl)
+// wraps (wmul = extent x stride, wlim = 1; one wrap suffices because the
+// 32-bit plan keeps |offset| <= extent for periodic dimensions; clamp and
+// unbounded dimensions have wmul = stride, wlim = INT32_MAX, and an
+// unbounded dimension is never left).  Straight-line arithmetic, the same
+// for every lane.
+__device__ __forceinline__ int32_t gather_fix(const GPt &r, uint32_t raw8, const int32_t (&wmul)[HPACML_MAX_RANK],
+                                              const int32_t (&wlim)[HPACML_MAX_RANK]) {
+    uint32_t fix = 0;   // modulo 2^32: the corrected index itself fits in int32
 #pragma unroll
-    for (int d = 0; d < HPACML_MAX_RANK; ++d)
-        if (__any(r.p[d] + m.word(HPACML_MW(omin) + d) < 0 ||
-                  r.p[d] + m.word(HPACML_MW(omax) + d) >= m.word(HPACML_MW(extent) + d)))
-            edge |= 1u << d;
-    return edge;
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        const int32_t o = (int32_t)(int8_t)(raw8 >> (8 * d));
+        const int32_t dl = min(max(o, r.lo[d]), r.hi[d]) - o;
+        fix += (uint32_t)min(max(dl, -wlim[d]), wlim[d]) * (uint32_t)wmul[d];
+    }
+    return (int32_t)fix;
 }
 
-// boundary correction of a feature with raw offsets raw8 (signed bytes) at
-// point r along the dimensions in `edge`: periodic wraps once, clamp
-// saturates; added to the interior element index
-__device__ __forceinline__ int32_t edge_fix_lm(const LaneMap &m, const Pt32 &r, uint32_t raw8, uint32_t edge) {
+// Boundary correction of the access with raw offsets raw8 (signed bytes,
+// wave-uniform) at point r, added to the interior element index; the same
+// straight-line arithmetic for every lane and every dimension, so that a
+// gather carries no branch and the compiler can interleave it with the
+// matrix instructions around it.  Per dimension, with q = coordinate +
+// offset and dl = clamp(q, 0, n - 1) - q (zero inside the array): clamp adds
+// dl strides; periodic adds sign(dl) * n strides, one wrap, which suffices
+// because the 32-bit plan keeps |offset| <= extent for periodic dimensions.
+// A dimension without a boundary mode is never left (the plan checks it),
+// and an unused dimension has extent 1 and offset 0: both add zero.
+__device__ __forceinline__ int32_t wrap_fix_lm(const LaneMap &m, const Pt32 &r, uint32_t raw8) {
     int32_t fix = 0;
 #pragma unroll
     for (int d = 0; d < HPACML_MAX_RANK; ++d) {
-        if (edge & (1u << d)) {
-            const int32_t q = r.p[d] + (int32_t)(int8_t)(raw8 >> (8 * d));
-            const int32_t n = m.word(HPACML_MW(extent) + d);
-            int32_t c;
-            if (m.word(HPACML_MW(bnd) + d) == HPACML_BND_PERIODIC)
-                c = (n & (q >> 31)) - (n & ~((q - n) >> 31));
-            else
-                c = max(0, min(q, n - 1)) - q;
-            fix += c * m.word(HPACML_MW(stride) + d);
-        }
+        const int32_t off = (int32_t)(int8_t)(raw8 >> (8 * d));
+        const int32_t n = m.word(HPACML_MW(extent) + d);
+        const int32_t st = m.word(HPACML_MW(stride) + d);
+        const bool per = m.word(HPACML_MW(bnd) + d) == HPACML_BND_PERIODIC;
+        const int32_t lim = per ? 1 : INT32_MAX;
+        const int32_t mul = per ? n * st : st;
+        const int32_t q = r.p[d] + off;
+        const int32_t dl = min(max(q, 0), n - 1) - q;
+        fix += min(max(dl, -lim), lim) * mul;
     }
     return fix;
 }
@@ -207,22 +238,39 @@ __device__ __forceinline__ void static_for(Fn &&fn) {
     }
 }
 
-// Tile geometry and the weight stream of one tile
+// Tile geometry and the weight stream of one tile.  The stream starts with
+// layer 1 interleaved with m-block 0 of the first hidden layer (the fused
+// region, padded to whole stages), in the order the kernel consumes them:
+// for each layer-1 m-block j its K-steps, then (j >= 2) K-steps 2j - 4 and
+// 2j - 3 of the hidden m-block 0; its last four K-steps close the region.
+// The hidden layers' other m-blocks follow, K-step by K-step.
+constexpr int fused_pos_l1(int ks1, int j, int s) { return j * ks1 + s + 2 * (j > 2 ? j - 2 : 0); }
+constexpr int fused_pos_h0(int ks1, int nmb, int k) {
+    return k < 2 * nmb - 4 ? (k / 2 + 3) * ks1 + k : nmb * ks1 + k;
+}
+
 template <int H, int NH, int KS1>
 struct RGeo {
     static constexpr int NMB = H / 32;                    // 32-feature m-blocks
     static constexpr int KS = H / 16;                     // K-steps of a hidden layer
     static constexpr int L1F = NMB * KS1;                 // first-layer fragments
-    static constexpr int L1S = (L1F + kSF - 1) / kSF;     // ... in whole stages
     static constexpr int HF = NMB * KS;                   // fragments of a hidden layer
-    static constexpr int ST = L1S + NH * HF / kSF;        // stages per tile
-    static_assert(HF % kSF == 0, "hidden layers are whole stages");
-    static_assert(KS % kR == 0 && (L1S * kSF) % kR == 0, "fragment registers aligned with the layers");
-    static_assert(NMB % 2 == 0, "m-blocks go in pairs");
+    static constexpr int FUSF = L1F + KS;                 // fused region: layer 1 + hidden m-block 0
+    static constexpr int FUS = (FUSF + kSF - 1) / kSF;    // ... in whole stages
+    static constexpr int ST = FUS + (NH * HF - KS) / kSF; // stages per tile
+    static constexpr int pos_l1(int j, int s) { return fused_pos_l1(KS1, j, s); }
+    static constexpr int pos_h0(int k) { return fused_pos_h0(KS1, NMB, k); }
+    // m-block j of hidden layer l (l = 0: j >= 1)
+    static constexpr int pos_h(int l, int j) { return FUS * kSF - KS + (l * NMB + j) * KS; }
+    static_assert(KS % kSF == 0, "hidden m-blocks are whole stages");
+    static_assert(KS % kR == 0 && (FUS * kSF) % kR == 0, "fragment registers aligned with the layers");
+    static_assert(NMB % 2 == 0 && NMB >= 4, "m-blocks go in pairs; the fused region needs four");
+    static_assert(KS > 7, "the epilogue of an m-block fits in the first eight K-steps of the next");
+    static_assert(pos_h0(KS - 1) == FUSF - 1, "the fused region is consumed in order");
     static_assert(H != 512 || NH == 1, "512-wide activations fill the accumulation registers: one hidden layer");
 };
 
-template <int H, int NH, int KS1, int GPS>
+template <int H, int NH, int KS1, int GPS, bool WIN>
 __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPacked pk, int32_t n_tiles) {
     using G = RGeo<H, NH, KS1>;
@@ -285,94 +333,123 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
     auto tile_of = [&](int it) { return lb + it * nb; };
 
     // gather of this wave's 64 points of a tile (lane = point), feature f
-    // into X buffer xb
-    auto gather_point = [&](int tile, Pt32 &pt, uint32_t &edge) {
+    // into X buffer xb; windowed maps (WIN) resolve boundaries per access
+    // (per-dimension constants of the map: wrap multiplier and sign limit)
+    int32_t wmul[HPACML_MAX_RANK], wlim[HPACML_MAX_RANK];
+#pragma unroll
+    for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+        const bool per = in.bnd[d] == HPACML_BND_PERIODIC;
+        wmul[d] = per ? (int32_t)((uint32_t)in.extent[d] * (uint32_t)in.stride[d]) : in.stride[d];
+        wlim[d] = per ? 1 : INT32_MAX;
+    }
+    auto gather_point = [&](int tile, GPt &gp) {
         int b = tile * kT + w * kP + lane;
         b = b < in.n_points ? b : in.n_points - 1;
         lin.fresh();
-        pt = locate_lm(lin, b);
-        edge = edge_dims_lm(lin, pt);
+        const Pt32 pt = locate_lm(lin, b);
+        gp.pe = pt.pe;
+        if constexpr (WIN) {
+#pragma unroll
+            for (int d = 0; d < HPACML_MAX_RANK; ++d) {
+                gp.lo[d] = -pt.p[d];
+                gp.hi[d] = lin.word(HPACML_MW(extent) + d) - 1 - pt.p[d];
+            }
+        }
     };
-    auto gather_one = [&](const Pt32 &pt, uint32_t edge, int f, int xb) {
+    auto gather_one = [&](const GPt &gp, int f, int xb) {
         const uint32_t lo = __builtin_amdgcn_readlane(t_lo, f), hi = __builtin_amdgcn_readlane(t_hi, f);
         const float *base = (const float *)(uintptr_t)(((uint64_t)hi << 32) | lo);
-        int32_t idx = pt.pe;
-        if (edge) {
-            lin.fresh();
-            idx += edge_fix_lm(lin, pt, __builtin_amdgcn_readlane(t_raw, f), edge);
-        }
+        int32_t idx = gp.pe;
+        if constexpr (WIN)
+            idx += gather_fix(gp, __builtin_amdgcn_readlane(t_raw, f), wmul, wlim);
         dma4(base + idx, lbase + (uint32_t)(xoff + xb * xbuf_bytes + xwave + f * 256));
     };
     // ring stage k (global count) from the tile stream into slot k % kNS
     const char *wsrc = (const char *)pk.stream + (size_t)(4 * w) * kFrag + (size_t)lane * 16;
-    auto ring_issue = [&](int k) {
+    // load i (of 4) of this wave's quarter of ring stage k
+    auto ring_part = [&](int k, int i) {
         const int q = k % ST, slot = k % kNS;
         const char *src = wsrc + (size_t)q * kStage;
         const uint32_t dst = lbase + (uint32_t)(slot * kStage + 4 * w * kFrag);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            dma16(src + i * kFrag, dst + i * kFrag);
+        dma16(src + i * kFrag, dst + i * kFrag);
     };
 
     // ---- prologue: the first two tiles' inputs, the first kD stages
     {
-        Pt32 pt;
-        uint32_t edge;
+        GPt gp;
         for (int i = 0; i < 2; ++i) {
             const int tt = tile_of(i) < n_tiles ? tile_of(i) : n_tiles - 1;
-            gather_point(tt, pt, edge);
+            gather_point(tt, gp);
             for (int f = 0; f < F; ++f)
-                gather_one(pt, edge, f, i);
+                gather_one(gp, f, i);
         }
         for (int k = 0; k < kD; ++k)
-            ring_issue(k);
+            for (int i = 0; i < 4; ++i)
+                ring_part(k, i);
         vm_wait<0>();
         block_barrier();
     }
 
-    Pt32 gpt;                        // gather point of tile it + 2
-    uint32_t gedge = 0;
+    GPt gpt;                         // gather point of tile it + 2
     int gx = 0;                      // its X buffer
     int kb = 0;                      // global stage index of this tile's first stage
     const u32x4 *fr_lane = smem + lane;
 
-    // publication of stage s + 1 of this tile (at fragment kSync of stage s):
-    // this wave's loads of it have landed, then every wave's; then the next
-    // loads go out (stage s + kD reuses the slot of stage s - 1, which every
-    // wave finished before the barrier)
-    auto sync = [&](int s) {
-        vm_wait<(kD - 2) * (GPS + 4)>();
-        block_barrier();
+    // Stage s of this tile, at fragment kSync: this wave's loads of stage
+    // s + 1 have landed, then (barrier) every wave's, so stage s + 1 is
+    // published.  The four loads of stage s + kD (into the slot of stage
+    // s - 1, which every wave finished reading before the barrier) go out
+    // at the next four fragments, the gathers of tile it + 2 at the fifth.
+    // Between two barriers a wave issues GPS + 4 loads, so at the barrier at
+    // most that many (the last stage's) may still be in flight.
+    auto stage_work = [&](auto PS, int s) {
+        constexpr int ps = decltype(PS)::value;
+        if constexpr (ps == kSync) {
+            vm_wait<(kD - 2) * (GPS + 4)>();
+            block_barrier();
+        } else if constexpr (ps > kSync && ps <= kSync + 4) {
+            ring_part(kb + s + kD, ps - kSync - 1);
+        } else if constexpr (ps == kSync + 5) {
 #pragma unroll
-        for (int i = 0; i < GPS; ++i) {
-            const int f = s * GPS + i;
-            gather_one(gpt, gedge, f < F ? f : F - 1, gx);
+            for (int i = 0; i < GPS; ++i) {
+                const int f = s * GPS + i;
+                gather_one(gpt, f < F ? f : F - 1, gx);
+            }
         }
-        ring_issue(kb + s + kD);
     };
     // the fragment pipeline: the read of the fragment at stream position
     // p + kPd is issued at position p (PC compile-time, pr a runtime multiple
-    // of kSF), after publishing the next stage when p + kPd enters it
+    // of kSF), after the stage work of position p
     u32x4 a[kR];
     auto frag_ptr = [&](int p) { return fr_lane + ((kb + p / kSF) % kNS) * (kStage / 16) + (p % kSF) * (kFrag / 16); };
     auto fragment = [&](auto PC, int pr) -> bf16x8 {
         constexpr int pc = decltype(PC)::value;
-        if constexpr (pc % kSF == kSync)
-            sync((pc + pr) / kSF);
+        stage_work(std::integral_constant<int, pc % kSF>{}, (pc + pr) / kSF);
         a[(pc + kPd) % kR] = *frag_ptr(pc + pr + kPd);
+        // keep the read kPd fragments ahead of its use: neither it nor the
+        // matrix instructions may be moved across this point (the scheduler
+        // would otherwise sink the read to just before its consumer and wait
+        // for it there); vector and scalar ALU work still moves freely
+        __builtin_amdgcn_sched_barrier(kSchedAluOnly);
         return as_bf16x8(a[pc % kR]);
     };
-    // K loop of one m-block: fragments at positions PC0 + pr + s, B operands
-    // hin[s], accumulators (c0, c1) from cinit (zero, or the layer's biases);
-    // mid(S) runs after K-step S (the previous m-block's epilogue, spread
-    // over the loop)
+    // one K-step: the fragment at position PC (+ pr) times the B operands
+    // b[0], b[1] into accumulators (c0, c1), which start from cinit when
+    // FIRST (zero, or the layer's biases)
+    auto kstep = [&](auto PC, int pr, const u32x4 (&b)[2], floatx16 &c0, floatx16 &c1, bool first,
+                     const floatx16 &cinit) {
+        const bf16x8 av = fragment(PC, pr);
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(b[0]), first ? cinit : c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(b[1]), first ? cinit : c1, 0, 0, 0);
+    };
+    // K loop of one m-block: K-step s at position PC0 + pr + s, B operands
+    // hin[s]; mid(S) runs after K-step S (the previous m-block's epilogue,
+    // spread over the loop)
     auto kloop = [&](auto PC0, int pr, auto NK, const u32x4 (*hin)[2], floatx16 &c0, floatx16 &c1,
                      const floatx16 &cinit, auto mid) {
         static_for<0, decltype(NK)::value>([&](auto S) {
             constexpr int s = decltype(S)::value;
-            const bf16x8 av = fragment(std::integral_constant<int, decltype(PC0)::value + s>{}, pr);
-            c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][0]), s == 0 ? cinit : c0, 0, 0, 0);
-            c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, as_bf16x8(hin[s][1]), s == 0 ? cinit : c1, 0, 0, 0);
+            kstep(std::integral_constant<int, decltype(PC0)::value + s>{}, pr, hin[s], c0, c1, s == 0, cinit);
             mid(S);
         });
     };
@@ -403,40 +480,62 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
 
     u32x4 h[NH > 1 ? 2 : 1][KS][2];  // activations: B fragments [K-step][n-block]
     floatx16 acc[2][2];
+    floatx16 hacc[2];                // m-block 0 of the first hidden layer
 
     for (int it = 0; tile_of(it) < n_tiles; ++it) {
         const int tile = tile_of(it);
         {
             int tg = tile_of(it + 2);
             tg = tg < n_tiles ? tg : n_tiles - 1;
-            gather_point(tg, gpt, gedge);
+            gather_point(tg, gpt);
             gx = it & 1;
         }
 
         // ---- this tile's inputs (X buffer it & 1) as layer-1 B fragments;
         //      features F..F+2 carry the first-layer bias
+        // Rows below 16 (KS1 - 1) - 2 (the fewest inputs of this K-step
+        // count) are inputs for every F; the others are read from a clamped
+        // row unconditionally and then masked without a branch: the input
+        // itself below F, 1 for the three bias columns, 0 above.
         u32x4 xb[KS1][2];
         {
+            constexpr int FMIN = 16 * (KS1 - 1) - 2;
             const float *xa = (const float *)(lds + xoff + (it & 1) * xbuf_bytes + xwave);
+            int32_t tb = 8 * g - F;                 // feature - F of element 0 of K-step 0 in this lane
+            asm volatile("" : "+v"(tb));
 #pragma unroll
             for (int s = 0; s < KS1; ++s)
 #pragma unroll
                 for (int n = 0; n < 2; ++n) {
-                    float v[8];
+                    uint32_t v[8];
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
-                        const int f = 16 * s + 8 * g + e;
-                        const int fc = f < F ? f : F - 1;
-                        const float x = xa[fc * 64 + 32 * n + col];
-                        v[e] = f < F ? x : (f < F + 3 ? 1.f : 0.f);
+                        const int f0 = 16 * s + e;
+                        if (16 * s + 8 + e < FMIN) {     // resolved at unrolling
+                            v[e] = __builtin_bit_cast(uint32_t, xa[(f0 + 8 * g) * 64 + 32 * n + col]);
+                        } else {
+                            const int32_t t = tb + f0;     // feature - F
+                            const int fc = t < 0 ? f0 + 8 * g : F - 1;
+                            uint32_t x = __builtin_bit_cast(uint32_t, xa[fc * 64 + 32 * n + col]);
+                            asm volatile("" : "+v"(x));
+                            const uint32_t real = (uint32_t)(t >> 31);               // t < 0
+                            const uint32_t one = (uint32_t)((t - 3) >> 31) & 0x3F800000u;  // t < 3
+                            v[e] = (x & real) | (one & ~real);
+                        }
                     }
-                    xb[s][n] = u32x4{pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])};
+                    xb[s][n] = u32x4{pack2(__builtin_bit_cast(float, v[0]), __builtin_bit_cast(float, v[1])),
+                                     pack2(__builtin_bit_cast(float, v[2]), __builtin_bit_cast(float, v[3])),
+                                     pack2(__builtin_bit_cast(float, v[4]), __builtin_bit_cast(float, v[5])),
+                                     pack2(__builtin_bit_cast(float, v[6]), __builtin_bit_cast(float, v[7]))};
                 }
         }
 
-        // ---- layer 1, m-block by m-block; the epilogue of m-block j - 1
-        //      (activation, bf16 -> K-steps 2j - 2, 2j - 1 of the next layer)
-        //      after the first K-step of m-block j
+        // ---- layer 1, fused with m-block 0 of the first hidden layer: for
+        //      each m-block j of layer 1, its K-steps, then the epilogue of
+        //      m-block j - 1 (activation, bf16 -> K-steps 2j - 2, 2j - 1 of
+        //      the next layer), then K-steps 2j - 4, 2j - 3 of the hidden
+        //      m-block 0, whose inputs the epilogue before made; the vector
+        //      work of each epilogue runs beside ten matrix instructions
         {
             auto epi1 = [&](auto J) {
                 constexpr int j = decltype(J)::value;
@@ -447,43 +546,59 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 });
             };
             const floatx16 zero = {};
+            const floatx16 b00 = bias_of(0, 0);
+            auto h0 = [&](auto K) {
+                constexpr int k = decltype(K)::value;
+                kstep(std::integral_constant<int, G::pos_h0(k)>{}, 0, h[0][k], hacc[0], hacc[1], k == 0, b00);
+            };
             static_for<0, NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
-                kloop(std::integral_constant<int, j * KS1>{}, 0, std::integral_constant<int, KS1>{}, xb,
-                      acc[j & 1][0], acc[j & 1][1], zero, [&](auto S) {
-                          if constexpr (decltype(S)::value == 0 && j > 0)
-                              epi1(std::integral_constant<int, (j > 0 ? j - 1 : 0)>{});
-                      });
+                static_for<0, KS1>([&](auto S) {
+                    constexpr int s = decltype(S)::value;
+                    kstep(std::integral_constant<int, G::pos_l1(j, s)>{}, 0, xb[s], acc[j & 1][0], acc[j & 1][1],
+                          s == 0, zero);
+                });
+                if constexpr (j >= 1)
+                    epi1(std::integral_constant<int, (j >= 1 ? j - 1 : 0)>{});
+                if constexpr (j >= 2) {
+                    h0(std::integral_constant<int, (j >= 2 ? 2 * j - 4 : 0)>{});
+                    h0(std::integral_constant<int, (j >= 2 ? 2 * j - 3 : 0)>{});
+                }
             });
-            // the first layer's padding fragments (its stages are whole)
-            static_for<G::L1F, G::L1S * kSF>([&](auto P) { (void)fragment(P, 0); });
             epi1(std::integral_constant<int, NMB - 1>{});
+            static_for<KS - 4, KS>([&](auto K) { h0(K); });
+            // padding fragments up to the stage boundary
+            static_for<G::FUSF, G::FUS * kSF>([&](auto P) { (void)fragment(P, 0); });
         }
 
         // ---- hidden layers before the last: m-blocks unrolled (their
-        //      activations land in statically indexed registers)
+        //      activations land in statically indexed registers); m-block 0
+        //      of layer 0 is done
         static_for<0, NH - 1>([&](auto L) {
             constexpr int l = decltype(L)::value;
             const u32x4(*hin)[2] = h[l % 2];
             u32x4(*hout)[2] = h[(l + 1) % 2];
-            auto epih = [&](auto J) {
+            auto epih = [&](auto J, floatx16 (&c)[2]) {
                 constexpr int j = decltype(J)::value;
                 static_for<0, 2>([&](auto T) {
                     constexpr int t = decltype(T)::value;
-                    hout[2 * j + t][0] = to_agpr(to_b(acc[j & 1][0], t));
-                    hout[2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t));
+                    hout[2 * j + t][0] = to_agpr(to_b(c[0], t));
+                    hout[2 * j + t][1] = to_agpr(to_b(c[1], t));
                 });
             };
-            static_for<0, NMB>([&](auto J) {
+            static_for<(l == 0 ? 1 : 0), NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
-                kloop(std::integral_constant<int, G::L1S * kSF + l * G::HF + j * KS>{}, 0,
-                      std::integral_constant<int, KS>{}, hin, acc[j & 1][0], acc[j & 1][1], bias_of(l, j),
-                      [&](auto S) {
-                          if constexpr (decltype(S)::value == 1 && j > 0)
-                              epih(std::integral_constant<int, (j > 0 ? j - 1 : 0)>{});
+                kloop(std::integral_constant<int, G::pos_h(l, j)>{}, 0, std::integral_constant<int, KS>{}, hin,
+                      acc[j & 1][0], acc[j & 1][1], bias_of(l, j), [&](auto S) {
+                          if constexpr (decltype(S)::value == 1 && j > 0) {
+                              if constexpr (l == 0 && j == 1)
+                                  epih(std::integral_constant<int, 0>{}, hacc);
+                              else
+                                  epih(std::integral_constant<int, (j > 0 ? j - 1 : 0)>{}, acc[(j - 1) & 1]);
+                          }
                       });
             });
-            epih(std::integral_constant<int, NMB - 1>{});
+            epih(std::integral_constant<int, NMB - 1>{}, acc[(NMB - 1) & 1]);
         });
 
         // ---- last hidden layer, streamed into the output layer: m-blocks in
@@ -493,7 +608,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
         {
             constexpr int l = NH - 1;
             const u32x4(*hin)[2] = h[l % 2];
-            using P0 = std::integral_constant<int, G::L1S * kSF + l * G::HF>;   // stream position of the layer
+            // stream position of m-block j is P0 + j KS (m-block 0 of a
+            // single hidden layer was fused with layer 1)
+            using P0 = std::integral_constant<int, G::pos_h(l, 0)>;
             using NKS = std::integral_constant<int, KS>;
             floatx16 y0 = {}, y1 = {};
             // part q of the epilogue of m-block j (accumulators c): K-step
@@ -520,12 +637,16 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                     }
                 });
             };
-            mblock(0, acc[0], acc[1], true);
-            for (int j = 1; j < NMB - 1; j += 2) {
-                mblock(j, acc[1], acc[0], false);
-                mblock(j + 1, acc[0], acc[1], false);
+            if constexpr (NH == 1) {
+                mblock(1, acc[1], hacc, false);
+            } else {
+                mblock(0, acc[0], acc[1], true);
+                mblock(1, acc[1], acc[0], false);
             }
-            mblock(NMB - 1, acc[1], acc[0], false);
+            for (int j = 2; j < NMB; j += 2) {
+                mblock(j, acc[0], acc[1], false);
+                mblock(j + 1, acc[1], acc[0], false);
+            }
             static_for<0, 4>([&](auto Q) { epi_part(Q, NMB - 1, acc[1]); });
 
             // ---- scatter: y rows are outputs (row 4 g + r in register r < 4),
@@ -536,10 +657,8 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 const int b = tile * kT + w * kP + 32 * n + col;
                 lout.fresh();
                 const Pt32 pt = locate_lm(lout, b < out.n_points ? b : out.n_points - 1);
-                const uint32_t edge = edge_dims_lm(lout, pt);
-                int32_t idx = pt.pe;
-                if (edge)
-                    idx += edge_fix_lm(lout, pt, o_raw, edge);
+                lout.fresh();
+                const int32_t idx = pt.pe + wrap_fix_lm(lout, pt, o_raw);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int o = r + 4 * g;
@@ -569,8 +688,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
 int b_feature(int s, int g, int e) { return 32 * (s / 2) + 16 * (s % 2) + 8 * (e / 4) + 4 * g + e % 4; }
 
 int ring_stages(int H, int n_hidden, int ks1) {
-    const int l1f = (H / 32) * ks1;
-    return (l1f + kSF - 1) / kSF + n_hidden * (H / 32) * (H / 16) / kSF;
+    const int nmb = H / 32, ks = H / 16;
+    const int fus = (nmb * ks1 + ks + kSF - 1) / kSF;
+    return fus + (n_hidden * nmb * ks - ks) / kSF;
 }
 
 // first-layer K-steps and gathers per ring stage of a shape
@@ -596,7 +716,12 @@ hipError_t launch_r(const Map32 &in, const Map32 &out, const FeatTable32 &tin, c
     if (hipGetDevice(&dev) == hipSuccess)
         (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     const int32_t grid = n_tiles < cus ? n_tiles : cus;
-    auto kern = mlp_bf16r_kernel<H, NH, KS1, GPS>;
+    // a map whose features all sit at the sweep point needs no boundary
+    // resolution in its gathers
+    bool win = false;
+    for (int d = 0; d < HPACML_MAX_RANK; ++d)
+        win = win || in.omin[d] != 0 || in.omax[d] != 0;
+    auto kern = win ? mlp_bf16r_kernel<H, NH, KS1, GPS, true> : mlp_bf16r_kernel<H, NH, KS1, GPS, false>;
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
@@ -640,7 +765,11 @@ void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const 
     const int NMB = H / 32, KS = H / 16, nh = n_layers - 2;
     const int ks1 = bf16r_ks1(F);
     const int st = ring_stages(H, nh, ks1);
-    const int l1s = (NMB * ks1 + kSF - 1) / kSF;
+    const int fus = (NMB * ks1 + KS + kSF - 1) / kSF;
+    // stream position of K-step s of m-block j of hidden layer h
+    auto pos_hidden = [&](int h, int j, int s) {
+        return h == 0 && j == 0 ? fused_pos_h0(ks1, NMB, s) : fus * kSF - KS + (h * NMB + j) * KS + s;
+    };
     std::vector<uint16_t> stream((size_t)st * kSF * 64 * 8, 0);
     auto put = [&](int pos, int l, int e, uint16_t v) { stream[((size_t)pos * 64 + l) * 8 + e] = v; };
     for (int j = 0; j < NMB; ++j)
@@ -656,7 +785,7 @@ void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const 
                         split_bias(b[0][o], t);
                         v = t[k - F];
                     }
-                    put(j * ks1 + s, l, e, v);
+                    put(fused_pos_l1(ks1, j, s), l, e, v);
                 }
     for (int h = 0; h < nh; ++h)
         for (int j = 0; j < NMB; ++j)
@@ -665,7 +794,7 @@ void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const 
                     for (int e = 0; e < 8; ++e) {
                         const int o = 32 * j + l % 32;
                         const int k = b_feature(s, l / 32, e);
-                        put(l1s * kSF + (h * NMB + j) * KS + s, l, e, bf16_rne_host(W[h + 1][(size_t)o * H + k]));
+                        put(pos_hidden(h, j, s), l, e, bf16_rne_host(W[h + 1][(size_t)o * H + k]));
                     }
     // output layer: m-block j, K-step t, lane half g, row i < 8 (16 bytes each)
     std::vector<uint16_t> w3((size_t)NMB * 2 * 2 * 8 * 8, 0);

@@ -333,6 +333,61 @@ def test_fast_kernels_input_widths(compute, H, F_in, F_out, want):
     assert_close(np.stack(got, 1), Y, RTOL[compute], var)
 
 
+@pytest.mark.parametrize("case", ["h512_rank3_clamp_periodic_strided", "h256_rank2_shifted_periodic_output"])
+def test_bf16r_window_boundaries(case):
+    """The register-resident bf16 kernel on windowed maps whose windows
+    leave the arrays along every dimension: clamp and periodic boundaries,
+    a sub-sweep that starts inside the array, strided target views, and (for
+    the 256-wide model) outputs written one row down with periodic wrap, so
+    the branch-free boundary arithmetic of both the gathers and the scatter
+    runs at every edge.  Several tiles per block and a ragged last tile."""
+    import torch
+    g = np.random.default_rng(2407)
+    if case.startswith("h512"):
+        bigs = [g.standard_normal((40, 64, 200)).astype(np.float32) for _ in range(2)]
+        views_np = [b[:, :, ::2] for b in bigs]
+        spec = {"rank": 3, "slices": [((-1, 0, -1), (3, 2, 3))], "sweep": ((1, 0, 3), (40, 64, 100), (1, 1, 1)),
+                "bnd": [wl.CLAMP, wl.PERIODIC, wl.CLAMP]}
+        F = oracle.n_features(spec, views_np)
+        assert F == 36
+        npts = oracle.n_points(spec, views_np)
+        dims, H, want = [F, 512, 512, 3], 512, "mlp_bf16r_h512"
+        out_spec = wl.pointwise_spec(npts)
+        outs_np = [wl.sentinel_like((npts,)) for _ in range(3)]
+        dev = [d[:, :, ::2] for d in to_dev(bigs)]
+    else:
+        ny, nx = 300, 500
+        views_np = [g.standard_normal((ny, nx)).astype(np.float32) for _ in range(2)]
+        spec = {"rank": 2, "slices": [((-1, -1), (2, 3))], "sweep": ((0, 0), (ny, nx), (1, 1)),
+                "bnd": [wl.PERIODIC, wl.CLAMP]}
+        F = oracle.n_features(spec, views_np)
+        assert F == 12
+        npts = ny * nx
+        dims, H, want = [F, 256, 256, 256, 2], 256, "mlp_bf16r_h256"
+        out_spec = {"rank": 2, "slices": [((1, 0), (1, 1))], "sweep": ((0, 0), (ny, nx), (1, 1)),
+                    "bnd": [wl.PERIODIC, wl.NONE]}
+        outs_np = [wl.sentinel_like((ny, nx)) for _ in range(2)]
+        dev = to_dev(views_np)
+    model = wl.make_model(90 + H // 256, dims, "bf16")
+    Y = oracle.infer_rows(spec, views_np, model)
+    exp = [o.copy() for o in outs_np]
+    oracle.scatter(out_spec, exp, Y)
+    outs = to_dev(outs_np)
+    mi = api.Map(spec, dev, _abi.TO)
+    mo = api.Map(out_spec, outs, _abi.FROM)
+    m = api.Model(model)
+    var = api.variant(m, mi, mo)
+    assert var == want, var
+    api.infer(m, mi, mo)
+    torch.cuda.synchronize()
+    got = np.stack([o.cpu().numpy().reshape(-1) for o in outs], 1)
+    expY = np.stack([a.reshape(-1) for a in exp], 1)
+    assert not np.any(got.view(np.uint32) == wl.SENTINEL_BITS), "unwritten output element"
+    worst, norm = assert_close(got, expY, RTOL["bf16"], "%s via %s" % (case, var))
+    print("%s [%s]: %d points, worst scaled %.3e, normwise %.3e" % (case, var, npts, worst, norm))
+    mi.close(), mo.close(), m.close()
+
+
 @pytest.mark.parametrize("compute", ["f32", "bf16"])
 def test_limits_max_features_targets_width(compute):
     """The ABI's maxima in one region: 64 input targets x a 2x2 clamped
