@@ -73,9 +73,9 @@ def log(msg):
     print("[bench] " + msg, file=sys.stderr, flush=True)
 
 
-def recorded_traffic(variant, workload):
-    """HBM bytes per launch of `variant` on `workload` from profiles/*.txt,
-    if the kernel source is unchanged since the counters were taken."""
+def source_sha(variant):
+    """Hash of the sources of the kernel family `variant` belongs to (the key
+    under which profiles/*.txt record its counters), or None."""
     fam = next((k for k in KERNEL_SOURCES if variant.startswith(k)), None)
     if fam is None:
         return None
@@ -85,7 +85,15 @@ def recorded_traffic(variant, workload):
         if not os.path.exists(path):
             return None
         h.update(open(path, "rb").read())
-    sha = h.hexdigest()[:16]
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic(variant, workload):
+    """HBM bytes per launch of `variant` on `workload` from profiles/*.txt,
+    if the kernel source is unchanged since the counters were taken."""
+    sha = source_sha(variant)
+    if sha is None:
+        return None
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.txt"))):
         for line in open(path):
             if line.startswith("traffic_line "):

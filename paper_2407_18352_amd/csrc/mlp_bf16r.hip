@@ -265,7 +265,7 @@ struct RGeo {
     static_assert(KS % kSF == 0, "hidden m-blocks are whole stages");
     static_assert(KS % kR == 0 && (FUS * kSF) % kR == 0, "fragment registers aligned with the layers");
     static_assert(NMB % 2 == 0 && NMB >= 4, "m-blocks go in pairs; the fused region needs four");
-    static_assert(KS > 7, "the epilogue of an m-block fits in the first eight K-steps of the next");
+    static_assert(KS > 14, "an m-block's K-steps hold the previous epilogue (1-7) and the output indices (10, 14)");
     static_assert(pos_h0(KS - 1) == FUSF - 1, "the fused region is consumed in order");
     static_assert(H != 512 || NH == 1, "512-wide activations fill the accumulation registers: one hidden layer");
 };
@@ -535,15 +535,14 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
         //      m-block j - 1 (activation, bf16 -> K-steps 2j - 2, 2j - 1 of
         //      the next layer), then K-steps 2j - 4, 2j - 3 of the hidden
         //      m-block 0, whose inputs the epilogue before made; the vector
-        //      work of each epilogue runs beside ten matrix instructions
+        //      work of each epilogue runs beside ten matrix instructions, one
+        //      quarter after each of its first four K-steps
         {
-            auto epi1 = [&](auto J) {
-                constexpr int j = decltype(J)::value;
-                static_for<0, 2>([&](auto T) {
-                    constexpr int t = decltype(T)::value;
-                    h[0][2 * j + t][0] = to_agpr(to_b(acc[j & 1][0], t));
-                    h[0][2 * j + t][1] = to_agpr(to_b(acc[j & 1][1], t));
-                });
+            // quarter q of the epilogue of layer-1 m-block j: K-step 2j + q / 2
+            // of the next layer, n-block q % 2
+            auto epi1 = [&](auto J, auto Q) {
+                constexpr int j = decltype(J)::value, q = decltype(Q)::value;
+                h[0][2 * j + q / 2][q % 2] = to_agpr(to_b(acc[j & 1][q % 2], q / 2));
             };
             const floatx16 zero = {};
             const floatx16 b00 = bias_of(0, 0);
@@ -553,20 +552,27 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             };
             static_for<0, NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
-                static_for<0, KS1>([&](auto S) {
-                    constexpr int s = decltype(S)::value;
-                    kstep(std::integral_constant<int, G::pos_l1(j, s)>{}, 0, xb[s], acc[j & 1][0], acc[j & 1][1],
-                          s == 0, zero);
+                constexpr int NK = KS1 + (j >= 2 ? 2 : 0);   // K-steps of this iteration
+                using JP = std::integral_constant<int, (j >= 1 ? j - 1 : 0)>;
+                static_for<0, NK>([&](auto I) {
+                    constexpr int i = decltype(I)::value;
+                    if constexpr (i < KS1)
+                        kstep(std::integral_constant<int, G::pos_l1(j, i)>{}, 0, xb[i], acc[j & 1][0], acc[j & 1][1],
+                              i == 0, zero);
+                    else
+                        h0(std::integral_constant<int, 2 * j - 4 + (i - KS1)>{});
+                    if constexpr (j >= 1 && i < 4)
+                        epi1(JP{}, I);
                 });
                 if constexpr (j >= 1)
-                    epi1(std::integral_constant<int, (j >= 1 ? j - 1 : 0)>{});
-                if constexpr (j >= 2) {
-                    h0(std::integral_constant<int, (j >= 2 ? 2 * j - 4 : 0)>{});
-                    h0(std::integral_constant<int, (j >= 2 ? 2 * j - 3 : 0)>{});
-                }
+                    static_for<(NK < 4 ? NK : 4), 4>([&](auto Q) { epi1(JP{}, Q); });
             });
-            epi1(std::integral_constant<int, NMB - 1>{});
-            static_for<KS - 4, KS>([&](auto K) { h0(K); });
+            // the last epilogue, each half before the K-step that needs it
+            using JL = std::integral_constant<int, NMB - 1>;
+            static_for<0, 4>([&](auto Q) {
+                epi1(JL{}, Q);
+                h0(std::integral_constant<int, KS - 4 + decltype(Q)::value>{});
+            });
             // padding fragments up to the stage boundary
             static_for<G::FUSF, G::FUS * kSF>([&](auto P) { (void)fragment(P, 0); });
         }
@@ -578,27 +584,27 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             constexpr int l = decltype(L)::value;
             const u32x4(*hin)[2] = h[l % 2];
             u32x4(*hout)[2] = h[(l + 1) % 2];
-            auto epih = [&](auto J, floatx16 (&c)[2]) {
-                constexpr int j = decltype(J)::value;
-                static_for<0, 2>([&](auto T) {
-                    constexpr int t = decltype(T)::value;
-                    hout[2 * j + t][0] = to_agpr(to_b(c[0], t));
-                    hout[2 * j + t][1] = to_agpr(to_b(c[1], t));
-                });
+            // quarter q of the epilogue of m-block j (accumulators c)
+            auto epih = [&](auto J, auto Q, floatx16 (&c)[2]) {
+                constexpr int j = decltype(J)::value, q = decltype(Q)::value;
+                hout[2 * j + q / 2][q % 2] = to_agpr(to_b(c[q % 2], q / 2));
             };
             static_for<(l == 0 ? 1 : 0), NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
                 kloop(std::integral_constant<int, G::pos_h(l, j)>{}, 0, std::integral_constant<int, KS>{}, hin,
                       acc[j & 1][0], acc[j & 1][1], bias_of(l, j), [&](auto S) {
-                          if constexpr (decltype(S)::value == 1 && j > 0) {
+                          constexpr int s = decltype(S)::value;
+                          if constexpr (s >= 1 && s <= 4 && j > 0) {
+                              using JP = std::integral_constant<int, (j > 0 ? j - 1 : 0)>;
+                              using Q = std::integral_constant<int, s - 1>;
                               if constexpr (l == 0 && j == 1)
-                                  epih(std::integral_constant<int, 0>{}, hacc);
+                                  epih(JP{}, Q{}, hacc);
                               else
-                                  epih(std::integral_constant<int, (j > 0 ? j - 1 : 0)>{}, acc[(j - 1) & 1]);
+                                  epih(JP{}, Q{}, acc[(j - 1) & 1]);
                           }
                       });
             });
-            epih(std::integral_constant<int, NMB - 1>{}, acc[(NMB - 1) & 1]);
+            static_for<0, 4>([&](auto Q) { epih(std::integral_constant<int, NMB - 1>{}, Q, acc[(NMB - 1) & 1]); });
         });
 
         // ---- last hidden layer, streamed into the output layer: m-blocks in
@@ -626,26 +632,45 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                     y0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wo, as_bf16x8(b0), y0, 0, 0, 0);
                 }
             };
+            // element index of this lane's output point of n-block n (the
+            // from map's boundary resolved), computed as vector filler
+            // during m-block 1
+            int32_t sidx[2];
+            auto scatter_index = [&](int n) {
+                const int b = tile * kT + w * kP + 32 * n + col;
+                lout.fresh();
+                const Pt32 pt = locate_lm(lout, b < out.n_points ? b : out.n_points - 1);
+                lout.fresh();
+                sidx[n] = pt.pe + wrap_fix_lm(lout, pt, o_raw);
+            };
             // m-block j into accumulators cur; the epilogue of m-block j - 1
-            // (accumulators prev) at K-steps 1, 3, 5, 7
-            auto mblock = [&](int j, floatx16 (&cur)[2], floatx16 (&prev)[2], bool first) {
+            // (accumulators prev) at K-steps 1, 3, 5, 7; extra(S) after K-step S
+            auto mblock = [&](int j, floatx16 (&cur)[2], floatx16 (&prev)[2], bool first, auto extra) {
                 kloop(P0{}, j * KS, NKS{}, hin, cur[0], cur[1], bias_of(l, j), [&](auto S) {
                     constexpr int s = decltype(S)::value;
                     if constexpr (s == 1 || s == 3 || s == 5 || s == 7) {
                         if (!first)
                             epi_part(std::integral_constant<int, (s >> 1)>{}, j - 1, prev);
                     }
+                    extra(S);
                 });
             };
+            auto none = [](auto) {};
+            auto indices = [&](auto S) {
+                if constexpr (decltype(S)::value == 10)
+                    scatter_index(0);
+                if constexpr (decltype(S)::value == 14)
+                    scatter_index(1);
+            };
             if constexpr (NH == 1) {
-                mblock(1, acc[1], hacc, false);
+                mblock(1, acc[1], hacc, false, indices);
             } else {
-                mblock(0, acc[0], acc[1], true);
-                mblock(1, acc[1], acc[0], false);
+                mblock(0, acc[0], acc[1], true, none);
+                mblock(1, acc[1], acc[0], false, indices);
             }
             for (int j = 2; j < NMB; j += 2) {
-                mblock(j, acc[0], acc[1], false);
-                mblock(j + 1, acc[1], acc[0], false);
+                mblock(j, acc[0], acc[1], false, none);
+                mblock(j + 1, acc[1], acc[0], false, none);
             }
             static_for<0, 4>([&](auto Q) { epi_part(Q, NMB - 1, acc[1]); });
 
@@ -655,10 +680,7 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             for (int n = 0; n < 2; ++n) {
                 const floatx16 &y = n ? y1 : y0;
                 const int b = tile * kT + w * kP + 32 * n + col;
-                lout.fresh();
-                const Pt32 pt = locate_lm(lout, b < out.n_points ? b : out.n_points - 1);
-                lout.fresh();
-                const int32_t idx = pt.pe + wrap_fix_lm(lout, pt, o_raw);
+                const int32_t idx = sidx[n];
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const int o = r + 4 * g;
