@@ -62,7 +62,8 @@ DESCRIPTION = {
 KERNEL_SOURCES = {
     "collect": ["collect.hip", "device.hpp", "kernels.hpp"],
     "mlp_f32": ["mlp_f32.hip", "device.hpp", "kernels.hpp"],
-    "mlp_bf16r": ["mlp_bf16r.hip", "device.hpp", "kernels.hpp"],
+    "mlp_bf16r": ["mlp_bf16r.hip", "mlp_bf16r.hpp", "mlp_bf16r_h256_nh1.hip", "mlp_bf16r_h256_nh2.hip",
+                  "mlp_bf16r_h256_nh3.hip", "device.hpp", "kernels.hpp"],
     "mlp_bf16": ["mlp_bf16.hip", "device.hpp", "kernels.hpp"],
     "mlp_generic": ["mlp_generic.hip", "device.hpp", "kernels.hpp"],
     "cnn_": ["cnn.hip", "cnn.hpp", "device.hpp", "kernels.hpp"],
@@ -158,6 +159,14 @@ class Run:
         self.is_cnn = name in wl.CNN_NAMES
         t0 = time.time()
         w = wl.make_cnn(name) if self.is_cnn else wl.make(name)
+        if getattr(args, "dims", None) and not self.is_cnn:
+            # another model of the workload's model space (same inputs and outputs)
+            dims = [int(x) for x in args.dims.split(",")]
+            if dims[0] != w.dims[0] or dims[-1] != w.dims[-1] or len(dims) < 2:
+                print("--dims must keep %d inputs and %d outputs" % (w.dims[0], w.dims[-1]), file=sys.stderr)
+                sys.exit(2)
+            w.dims = dims
+            w.model = wl.make_model(w.cfg, dims, w.compute)
         self.w = w
         log("workload %s generated in %.1fs" % (name, time.time() - t0))
 
@@ -429,6 +438,9 @@ def main():
                     help="measure this workload alone (default: the 3-D stencil, with the other four MLP "
                          "workloads under configs)")
     ap.add_argument("--no-configs", action="store_true", help="skip the other workloads")
+    ap.add_argument("--dims", default=None,
+                    help="layer widths of another model for the workload, e.g. 6,1024,512,256,1 (inputs and "
+                         "outputs as the workload's; seeded He-normal weights)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-rotate", action="store_true",
                     help="keep every step on the same arrays even when they fit the Infinity Cache")
@@ -467,7 +479,7 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     name = args.workload or HEADLINE
-    with_configs = args.workload is None and not args.no_configs
+    with_configs = args.workload is None and not args.no_configs and not args.dims
     if args.inplace:
         args.no_cpu_baseline = True
 
@@ -499,7 +511,8 @@ def main():
         "dtype": run.w.compute,
         "data": "synthetic (seeded generators; random-init He-normal weights)",
         "config": {"workload": DESCRIPTION[name] + ("; outputs written in place into the input fields"
-                                                     if args.inplace else ""),
+                                                     if args.inplace else "")
+                   + ("; model %s instead" % "-".join(str(d) for d in run.w.dims) if args.dims else ""),
                    "points": B, "features_in": Fi, "features_out": Fo, "output_points": Bo},
         "roofline": roof,
         "infer_points_per_s": B / (run.infer_avg * 1e-3),

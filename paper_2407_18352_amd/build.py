@@ -35,7 +35,8 @@ DEVICE = ["-x", "hip", "--offload-arch=" + ARCH, "-Xclang", "-target-feature", "
 
 # the register-resident bf16 kernel keeps its activations in accumulation
 # registers as MFMA B operands; results and C operands go to vector registers
-PER_FILE = {"mlp_bf16r.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+PER_FILE = {f: ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+            for f in ("mlp_bf16r.hip", "mlp_bf16r_h256_nh1.hip", "mlp_bf16r_h256_nh2.hip", "mlp_bf16r_h256_nh3.hip")}
 
 
 def build(verbose: bool = False) -> str:

@@ -51,6 +51,8 @@ struct hpacml_model_s {
     BF16Packed bf16{};
     uint8_t *bf16r_buf = nullptr;    // weight stream, output fragments, biases of the register-resident bf16 kernel
     BF16RPacked bf16r{};
+    bool padded = false;             // the fast kernel runs the hidden layers zero-padded to its width
+    std::string fast_name;           // its name (with "_padded" then)
     // convolutional models
     bool cnn = false;
     CnnPlan cnnp;
@@ -345,6 +347,44 @@ hpacml_status check_collect(const hpacml_map *m, float *dst, int64_t ld) {
     return HPACML_OK;
 }
 
+// Hidden layers narrower than a fast kernel's uniform width H, zero-padded
+// to it: the added neurons have zero weights and a zero bias, so their
+// activation (ReLU or identity of 0) is 0 and, multiplied by the zero
+// weights of the next layer, adds nothing to it; the padded model computes
+// the unpadded one's sums (an infinite or NaN activation would turn a padded
+// weight's 0 into NaN).  Returns false when a hidden layer is wider than H.
+struct PaddedModel {
+    std::vector<int32_t> dims;
+    std::vector<std::vector<float>> W, b;
+    std::vector<const float *> Wp, bp;
+};
+bool pad_hidden(int n_layers, const int32_t *dims, const float *const *W, const float *const *b, int H,
+                PaddedModel &p) {
+    p.dims.assign(dims, dims + n_layers + 1);
+    for (int l = 1; l < n_layers; ++l) {
+        if (dims[l] > H)
+            return false;
+        p.dims[l] = H;
+    }
+    p.W.assign(n_layers, {});
+    p.b.assign(n_layers, {});
+    p.Wp.assign(n_layers, nullptr);
+    p.bp.assign(n_layers, nullptr);
+    for (int l = 0; l < n_layers; ++l) {
+        const int fi = dims[l], fo = dims[l + 1], pi = p.dims[l], po = p.dims[l + 1];
+        p.W[l].assign((size_t)po * pi, 0.f);
+        p.b[l].assign((size_t)po, 0.f);
+        for (int o = 0; o < fo; ++o) {
+            for (int i = 0; i < fi; ++i)
+                p.W[l][(size_t)o * pi + i] = W[l][(size_t)o * fi + i];
+            p.b[l][o] = b[l][o];
+        }
+        p.Wp[l] = p.W[l].data();
+        p.bp[l] = p.b[l].data();
+    }
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -536,27 +576,47 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
             m->gen.b[l] = m->gen_buf + boff[l];
         }
 
-        if (f32_fast_supported(n_layers, dims, compute)) {
-            std::vector<float> img(f32_image_floats(n_layers, dims), 0.f);
-            f32_pack(n_layers, dims, W, b, img.data());
+        // the fast kernels take uniform hidden widths; narrower or uneven
+        // hidden layers run padded to the smallest width a kernel has
+        int maxh = 0;
+        for (int l = 1; l < n_layers; ++l)
+            maxh = dims[l] > maxh ? dims[l] : maxh;
+        const int H = bf16 ? (maxh <= 256 ? 256 : (maxh <= 512 ? 512 : 0))
+                           : (maxh <= 64 ? 64 : (maxh <= 128 ? 128 : 0));
+        PaddedModel pm;
+        const int32_t *fd = dims;
+        const float *const *fW = W;
+        const float *const *fb = b;
+        if (n_layers >= 2 && H > 0 && pad_hidden(n_layers, dims, W, b, H, pm)) {
+            fd = pm.dims.data();
+            fW = pm.Wp.data();
+            fb = pm.bp.data();
+            for (int l = 1; l < n_layers; ++l)
+                m->padded = m->padded || dims[l] != H;
+        }
+
+        if (f32_fast_supported(n_layers, fd, compute)) {
+            std::vector<float> img(f32_image_floats(n_layers, fd), 0.f);
+            f32_pack(n_layers, fd, fW, fb, img.data());
             s = upload(&m->f32_img, img.data(), img.size());
             if (s != HPACML_OK) {
                 hpacml_model_destroy(m);
                 return s;
             }
-            m->f32.hid = dims[1];
+            m->f32.hid = fd[1];
             m->f32.n_hidden = n_layers - 2;
-            m->f32.ks1 = (dims[0] + 1) / 2;
-            m->f32.f_out = dims[n_layers];
+            m->f32.ks1 = (fd[0] + 1) / 2;
+            m->f32.f_out = fd[n_layers];
             for (int l = 0; l < n_layers; ++l)
                 m->f32.act[l] = act[l];
             m->f32.lds_bytes = (int32_t)(img.size() * sizeof(float));
             m->f32.image = m->f32_img;
             m->variant = Variant::F32;
-        } else if (bf16r_supported(n_layers, dims, act, compute)) {
+            m->fast_name = f32_variant_name(m->f32);
+        } else if (bf16r_supported(n_layers, fd, act, compute)) {
             std::vector<uint8_t> buf;
             size_t off_w3 = 0, off_bias = 0;
-            bf16r_pack(n_layers, dims, W, b, buf, &off_w3, &off_bias, &m->bf16r);
+            bf16r_pack(n_layers, fd, fW, fb, buf, &off_w3, &off_bias, &m->bf16r);
             s = upload(&m->bf16r_buf, buf.data(), buf.size());
             if (s != HPACML_OK) {
                 hpacml_model_destroy(m);
@@ -568,9 +628,10 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
             m->bf16r.w3 = m->bf16r_buf + off_w3;
             m->bf16r.bias = (const float *)(m->bf16r_buf + off_bias);
             m->variant = Variant::BF16R;
-        } else if (bf16_fast_supported(n_layers, dims, compute)) {
+            m->fast_name = bf16r_variant_name(m->bf16r);
+        } else if (bf16_fast_supported(n_layers, fd, compute)) {
             std::vector<uint16_t> frags;
-            bf16_pack(n_layers, dims, W, b, frags, &m->bf16);
+            bf16_pack(n_layers, fd, fW, fb, frags, &m->bf16);
             s = upload(&m->bf16_frags, frags.data(), frags.size());
             if (s != HPACML_OK) {
                 hpacml_model_destroy(m);
@@ -580,7 +641,12 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
                 m->bf16.act[l] = act[l];
             m->bf16.frags = m->bf16_frags;
             m->variant = Variant::BF16;
+            m->fast_name = bf16_variant_name(m->bf16);
         }
+        if (m->variant == Variant::Generic)
+            m->padded = false;
+        else if (m->padded)
+            m->fast_name += "_padded";
         *out = m;
         return HPACML_OK;
     } catch (const std::bad_alloc &) {
@@ -908,12 +974,9 @@ bool snapshot_t32(const hpacml_map *in) {
 
 // the kernel the dispatch below picks; `fast` = both maps take the 32-bit form
 const char *kernel_name(const hpacml_model *model, bool fast) {
-    switch (fast ? model->variant : Variant::Generic) {
-    case Variant::F32: return f32_variant_name(model->f32);
-    case Variant::BF16: return bf16_variant_name(model->bf16);
-    case Variant::BF16R: return bf16r_variant_name(model->bf16r);
-    default: return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
-    }
+    if (fast && model->variant != Variant::Generic)
+        return model->fast_name.c_str();
+    return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
 }
 
 // Every input of `in` into its snapshot record (stream-ordered before what

@@ -310,7 +310,8 @@ def test_infer_fast_paths_are_used():
     ("f32", 64, 5, 1, "mlp_f32_h64_k16"), ("f32", 64, 33, 3, "mlp_f32_h64_k40"),
     ("f32", 64, 57, 8, "mlp_f32_h64_k64"), ("f32", 128, 16, 2, "mlp_f32_h128_k16"),
     ("f32", 128, 40, 4, "mlp_f32_h128_k40"), ("f32", 128, 64, 1, "mlp_f32_h128_k64"),
-    ("bf16", 256, 13, 16, "mlp_bf16_h256"), ("bf16", 512, 7, 2, "mlp_bf16_h512"),
+    ("bf16", 256, 13, 16, "mlp_bf16_h256"), ("bf16", 512, 7, 12, "mlp_bf16_h512"),
+    ("bf16", 512, 7, 2, "mlp_bf16r_h512"), ("bf16", 512, 20, 3, "mlp_bf16r_h512"),
     ("bf16", 512, 45, 5, "mlp_bf16_h512"), ("bf16", 512, 61, 9, "mlp_bf16_h512"),
     ("bf16", 512, 35, 5, "mlp_bf16r_h512"), ("bf16", 512, 30, 8, "mlp_bf16r_h512"),
     ("bf16", 512, 42, 1, "mlp_bf16r_h512")])
@@ -386,6 +387,37 @@ def test_bf16r_window_boundaries(case):
     worst, norm = assert_close(got, expY, RTOL["bf16"], "%s via %s" % (case, var))
     print("%s [%s]: %d points, worst scaled %.3e, normwise %.3e" % (case, var, npts, worst, norm))
     mi.close(), mo.close(), m.close()
+
+
+@pytest.mark.parametrize("compute, dims, want", [
+    ("f32", [9, 96, 40, 1], "mlp_f32_h128_k16_padded"),          # bonds space: hidden 2 != hidden 1
+    ("f32", [5, 50, 20, 1], "mlp_f32_h64_k16_padded"),           # options space
+    ("f32", [36, 128, 100, 4], "mlp_f32_h128_k40_padded"),
+    ("f32", [9, 128, 128, 1], "mlp_f32_h128_k16"),               # uniform: not padded
+    ("bf16", [6, 256, 128, 64, 1], "mlp_bf16r_h256_padded"),     # MiniBUDE space: tapered, multiplier 0.5
+    ("bf16", [10, 256, 192, 128, 64, 1], "mlp_bf16r_h256_padded"),
+    ("bf16", [35, 400, 300, 5], "mlp_bf16r_h512_padded"),
+    ("bf16", [17, 160, 100, 3], "mlp_bf16r_h256_padded"),         # one hidden-to-hidden layer
+    ("bf16", [6, 200, 1], "mlp_bf16_h256_padded"),
+    ("bf16", [6, 1024, 512, 256, 1], "mlp_generic_bf16"),        # wider than 512: the general kernel
+])
+def test_padded_hidden_layers(compute, dims, want):
+    """Models whose hidden layers are uneven or narrower than a fast kernel's
+    width run on that kernel with the hidden layers zero-padded (the added
+    neurons have zero weights and bias): outputs against the oracle of the
+    unpadded model.  Several tiles per block and a ragged last tile."""
+    n = 70001 if compute == "bf16" else 140001
+    g = np.random.default_rng(sum(dims) * 7 + len(dims))
+    spec = wl.pointwise_spec(n)
+    w = wl.Workload("padded", 0, compute, dims, spec, spec,
+                    [g.uniform(-1, 1, n).astype(np.float32) for _ in range(dims[0])],
+                    [wl.sentinel_like((n,)) for _ in range(dims[-1])])
+    w.model = wl.make_model(50 + len(dims), dims, compute)
+    got, var = run_infer(w)
+    assert var == want, var
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    worst, norm = assert_close(np.stack(got, 1), Y, RTOL[compute], var)
+    print("%s %s [%s]: worst scaled %.3e normwise %.3e" % (compute, dims, var, worst, norm))
 
 
 @pytest.mark.parametrize("compute", ["f32", "bf16"])
@@ -485,31 +517,33 @@ def test_determinism_and_batch_order():
 
 @pytest.mark.parametrize("compute", ["f32", "bf16"])
 def test_generic_shapes_rank3_clamp_strided(compute):
-    """Shapes outside the MFMA kernels: uneven widths, rank-3 clamp/periodic
-    map with steps, strided target views."""
+    """A rank-3 clamp/periodic map with steps over strided target views, with
+    a hidden layer wider than the MFMA kernels take (the general kernel) and
+    with uneven narrow hidden layers (an MFMA kernel, zero-padded)."""
     import torch
     g = np.random.default_rng(77)
-    shape = (9, 11, 14)
     spec = {"rank": 3, "slices": [((-1, 0, 0), (3, 1, 1)), ((0, -2, 1), (1, 2, 2))],
             "sweep": ((1, 0, 2), (9, 11, 13), (2, 1, 3)), "bnd": [wl.CLAMP, wl.PERIODIC, wl.CLAMP]}
     bigs = [g.standard_normal((9, 11, 28)).astype(np.float32) for _ in range(2)]
     views = [b[:, :, ::2] for b in bigs]
     F = oracle.n_features(spec, views)
-    dims = [F, 40, 24, 3]
-    model = wl.make_model(9, dims, compute)
     npts = oracle.n_points(spec, views)
-    outs_np = [wl.sentinel_like((npts,)) for _ in range(3)]
-    Y = oracle.infer_rows(spec, views, model)
-    dev = [d[:, :, ::2] for d in to_dev(bigs)]
-    outs = to_dev(outs_np)
-    mi = api.Map(spec, dev, _abi.TO)
-    mo = api.Map(wl.pointwise_spec(npts), outs, _abi.FROM)
-    m = api.Model(model)
-    assert api.variant(m, mi, mo).startswith("mlp_generic")
-    api.infer(m, mi, mo)
-    torch.cuda.synchronize()
-    got = np.stack([o.cpu().numpy() for o in outs], 1)
-    assert_close(got, Y, RTOL[compute], "generic " + compute)
+    wide = 200 if compute == "f32" else 600
+    for dims, want in (([F, wide, 24, 3], "mlp_generic"), ([F, 40, 24, 3], "mlp_" + compute)):
+        model = wl.make_model(9, dims, compute)
+        outs_np = [wl.sentinel_like((npts,)) for _ in range(3)]
+        Y = oracle.infer_rows(spec, views, model)
+        dev = [d[:, :, ::2] for d in to_dev(bigs)]
+        outs = to_dev(outs_np)
+        mi = api.Map(spec, dev, _abi.TO)
+        mo = api.Map(wl.pointwise_spec(npts), outs, _abi.FROM)
+        m = api.Model(model)
+        var = api.variant(m, mi, mo)
+        assert var.startswith(want), var
+        api.infer(m, mi, mo)
+        torch.cuda.synchronize()
+        got = np.stack([o.cpu().numpy() for o in outs], 1)
+        assert_close(got, Y, RTOL[compute], "%s %s" % (var, dims))
 
 
 # ------------------------------------------------------------------ errors
