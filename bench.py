@@ -66,6 +66,7 @@ KERNEL_SOURCES = {
                   "mlp_bf16r_h256_nh3.hip", "device.hpp", "kernels.hpp"],
     "mlp_bf16": ["mlp_bf16.hip", "device.hpp", "kernels.hpp"],
     "mlp_generic": ["mlp_generic.hip", "device.hpp", "kernels.hpp"],
+    "mlp_layers": ["mlp_layers.hip", "layers.hpp", "device.hpp"],
     "cnn_": ["cnn.hip", "cnn.hpp", "device.hpp", "kernels.hpp"],
 }
 

@@ -19,9 +19,10 @@
  * that fails writes nothing.  `*out` handles are set to NULL on failure.
  *
  * Thread safety: maps and models are immutable after creation, except for
- * two buffers allocated on first need and reused: a `to` map's snapshot
- * record (inferences whose outputs overlap their inputs) and a convolutional
- * model's workspace (its layer-by-layer path).  Concurrent infer and collect
+ * buffers allocated on first need and reused: a `to` map's snapshot record
+ * (inferences whose outputs overlap their inputs) and a model's workspace
+ * (the layer-by-layer paths of convolutional models and of multilayer
+ * perceptrons outside the fused kernels).  Concurrent infer and collect
  * calls with the same handles on different streams are allowed, except that
  * calls using one of those buffers must not overlap in time.  A region is
  * used from one thread at a time, and its accurate path must not call
@@ -171,7 +172,23 @@ hpacml_status hpacml_model_validate(int32_t n_layers, const int32_t *dims,
  *            inputs and hidden activations rounded to bf16, nearest-even;
  *            fp32 accumulation; fp32 biases and outputs).
  * The weights are copied (and converted) into library-owned device memory;
- * the caller may free its host arrays on return.  Synchronises the device. */
+ * the caller may free its host arrays on return.  Synchronises the device.
+ * hpacml_infer runs the whole model in one fused kernel when both maps take
+ * the library's 32-bit form and the model fits one of its MFMA kernels
+ * (hidden widths up to 128 for fp32, up to 512 for bf16, with limits on
+ * depth, input features and outputs per kernel; hidden layers narrower than
+ * the kernel's width run zero-padded, which changes no result).  Any
+ * other model or map runs layer by layer: a gather kernel, one hipBLASLt
+ * matmul per layer (bias and activation applied to the fp32 accumulators in
+ * its epilogue; the same rounding points), a scatter kernel, over chunks of
+ * points.  That path uses a workspace the model owns (allocated on the first
+ * such call, grown as needed, freed with the model): two activation buffers
+ * of one chunk (about 256 MB each; the environment variable
+ * HPACML_LAYERS_CHUNK_MB, read when the model is created, sets another size),
+ * the chunk's fp32 outputs and up to 64 MB of library scratch; calls that
+ * share such a model must not overlap in time on different streams, and the
+ * first call must not be made under stream capture.  Where the library has
+ * no algorithm for a layer, a general fused VALU kernel runs instead. */
 hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims,
                                   const float *const *W, const float *const *b,
                                   const int32_t *act, int32_t compute,
@@ -364,7 +381,10 @@ void hpacml_region_destroy(hpacml_region *region);
  * capture, tight serving loops, harnesses that forbid hipMalloc.
  *
  * hpacml_infer_noalloc computes exactly what hpacml_infer computes, with the
- * same kernels, and allocates nothing (no hipMalloc / hipFree, no host heap).
+ * same kernels, and allocates nothing (no hipMalloc / hipFree, no host heap),
+ * except where hpacml_infer runs a multilayer perceptron layer by layer (it
+ * needs a workspace): there this entry point runs the general fused kernel,
+ * which has the same rounding points and another summation order.
  * Where hpacml_infer would copy the inputs into the `to` map's snapshot
  * record first (outputs that may overwrite inputs other points still read),
  * this entry point puts that record in a fixed scratch array of
@@ -384,8 +404,11 @@ hpacml_status hpacml_infer_noalloc(const hpacml_model *model, const hpacml_map *
                                    const hpacml_map *out, void *stream);
 
 /* Name of the kernel hpacml_infer would launch for these handles (a static
- * string, prefixed "snapshot+" when the inputs are copied first), or NULL
- * when the arguments are invalid.  Allocates nothing. */
+ * string, prefixed "snapshot+" when the inputs are copied first; the
+ * layer-by-layer path is "mlp_layers_f32" / "mlp_layers_bf16"), or NULL when
+ * the arguments are invalid.  Allocates no device buffer; for a model that
+ * runs layer by layer it selects the matmul library's algorithms for this
+ * point count (host work, cached with the model). */
 const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in,
                                  const hpacml_map *out);
 

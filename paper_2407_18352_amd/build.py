@@ -65,7 +65,8 @@ def build(verbose: bool = False) -> str:
             sys.stderr.write("FAILED: %s\n%s\n" % (c, t))
         raise RuntimeError("HIP build failed")
     tmp = OUT + ".tmp%d" % os.getpid()
-    link = [hipcc, "-shared", "-fPIC", "--hip-link", "--offload-arch=" + ARCH] + objs + ["-o", tmp]
+    # hipBLASLt: the per-layer matmuls of the layer-by-layer path
+    link = [hipcc, "-shared", "-fPIC", "--hip-link", "--offload-arch=" + ARCH] + objs + ["-lhipblaslt", "-o", tmp]
     res = subprocess.run(link, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
     if res.returncode != 0:
         sys.stderr.write(res.stdout.decode(errors="replace"))

@@ -12,6 +12,7 @@
 #include "hpacml.h"
 #include "cnn.hpp"
 #include "kernels.hpp"
+#include "layers.hpp"
 #include "plan.hpp"
 
 using namespace hpacml;
@@ -52,6 +53,7 @@ struct hpacml_model_s {
     uint8_t *bf16r_buf = nullptr;    // weight stream, output fragments, biases of the register-resident bf16 kernel
     BF16RPacked bf16r{};
     bool padded = false;             // the fast kernel runs the hidden layers zero-padded to its width
+    LayersPlan *layers = nullptr;    // layer-by-layer path (matmul library), in place of the general kernel
     std::string fast_name;           // its name (with "_padded" then)
     // convolutional models
     bool cnn = false;
@@ -514,6 +516,7 @@ void hpacml_model_destroy(hpacml_model *m) {
     (void)hipFree(m->cnn_buf);
     (void)hipFree(m->fused_buf);
     (void)hipFree(m->ws);
+    layers_destroy(m->layers);
     delete m;
 }
 
@@ -564,6 +567,13 @@ hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims, const f
         if (s != HPACML_OK) {
             hpacml_model_destroy(m);
             return s;
+        }
+        {
+            const hipError_t e = layers_create(n_layers, dims, act, W, b, compute, &m->layers);
+            if (e != hipSuccess) {
+                hpacml_model_destroy(m);
+                return hip_status(e);
+            }
         }
         m->gen.n_layers = n_layers;
         m->gen.bf16 = bf16 ? 1 : 0;
@@ -973,10 +983,23 @@ bool snapshot_t32(const hpacml_map *in) {
 }
 
 // the kernel the dispatch below picks; `fast` = both maps take the 32-bit form
-const char *kernel_name(const hpacml_model *model, bool fast) {
+const char *kernel_name(const hpacml_model *model, bool fast, int64_t n_points) {
     if (fast && model->variant != Variant::Generic)
         return model->fast_name.c_str();
+    if (layers_ready(model->layers, n_points))
+        return layers_name(model->layers);
     return model->compute == HPACML_BF16 ? "mlp_generic_bf16" : "mlp_generic_f32";
+}
+
+// The general path of hpacml_infer: layer by layer through the matmul
+// library, or the general fused kernel where the library has no algorithm.
+hipError_t launch_general(const hpacml_model *model, const DevMap &in, const DevMap &out, hipStream_t st) {
+    if (model->layers) {
+        const hipError_t e = layers_infer(model->layers, in, out, st);
+        if (e != hipErrorNotSupported)
+            return e;
+    }
+    return launch_mlp_generic(in, out, model->gen, st);
 }
 
 // Every input of `in` into its snapshot record (stream-ordered before what
@@ -1078,8 +1101,8 @@ const char *hpacml_infer_variant(const hpacml_model *model, const hpacml_map *in
                : cnn_fused_on_snapshot(model, in, out) ? "snapshot+cnn_fused_f32"
                                                        : "cnn_layers_f32";
     if (!snapshot)
-        return kernel_name(model, in->t32 && out->t32);
-    return snapshot_name(kernel_name(model, snapshot_t32(in) && out->t32));
+        return kernel_name(model, in->t32 && out->t32, in->plan.n_points);
+    return snapshot_name(kernel_name(model, snapshot_t32(in) && out->t32, in->plan.n_points));
 }
 
 hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, const hpacml_map *out,
@@ -1109,7 +1132,7 @@ hpacml_status hpacml_infer(const hpacml_model *model, const hpacml_map *in, cons
     case Variant::F32: e = launch_mlp_f32(in->m32, out->m32, in->tab, out->tab, model->f32, st); break;
     case Variant::BF16: e = launch_mlp_bf16(in->m32, out->m32, in->tab, out->tab, model->bf16, st); break;
     case Variant::BF16R: e = launch_mlp_bf16r(in->m32, out->m32, in->tab, out->tab, model->bf16r, st); break;
-    default: e = launch_mlp_generic(in->dev, out->dev, model->gen, st); break;
+    default: e = launch_general(model, in->dev, out->dev, st); break;
     }
     return hip_status(e);
 }

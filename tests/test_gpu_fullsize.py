@@ -140,3 +140,23 @@ def test_inplace_step_fullsize_sampled(name):
     worst, norm = assert_close(gotY, Y, RTOL[w.compute], "%s in place via %s" % (name, var))
     print("%s in place [%s] full size: worst %.3e normwise %.3e" % (name, var, worst, norm))
     del mi, mo, m
+
+
+def test_layers_path_fullsize_sampled():
+    """The 4,194,304 poses through a 6-1024-512-256-1 bf16 model, wider than
+    the fused kernels take: layer by layer at the default chunk size (32
+    chunks of 131,072 points), in the configuration the benchmark's --dims
+    run times; 2^14 seeded poses plus the first and last against the oracle."""
+    w = wl.make("poses")
+    w.dims = [6, 1024, 512, 256, 1]
+    w.model = wl.make_model(w.cfg, w.dims, w.compute)
+    got, var = run_infer(w)
+    assert var == "mlp_layers_bf16", var
+    rows = wl.sample_rows(w.n_points, 1 << 14, must=np.array([0, w.n_points - 1], np.int64))
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model, rows)
+    gotY = np.stack([a.reshape(-1)[rows] for a in got], 1)
+    worst, norm = assert_close(gotY, Y, RTOL["bf16"], "poses wide via " + var)
+    print("poses 6-1024-512-256-1 [%s]: %d sampled points, worst scaled %.3e normwise %.3e"
+          % (var, len(rows), worst, norm))
+    for a in got:
+        assert not np.any(a.view(np.uint32) == wl.SENTINEL_BITS), "unwritten output element"

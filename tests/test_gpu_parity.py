@@ -399,7 +399,7 @@ def test_bf16r_window_boundaries(case):
     ("bf16", [35, 400, 300, 5], "mlp_bf16r_h512_padded"),
     ("bf16", [17, 160, 100, 3], "mlp_bf16r_h256_padded"),         # one hidden-to-hidden layer
     ("bf16", [6, 200, 1], "mlp_bf16_h256_padded"),
-    ("bf16", [6, 1024, 512, 256, 1], "mlp_generic_bf16"),        # wider than 512: the general kernel
+    ("bf16", [6, 1024, 512, 256, 1], "mlp_layers_bf16"),         # wider than 512: layer by layer
 ])
 def test_padded_hidden_layers(compute, dims, want):
     """Models whose hidden layers are uneven or narrower than a fast kernel's
@@ -424,7 +424,7 @@ def test_padded_hidden_layers(compute, dims, want):
 def test_limits_max_features_targets_width(compute):
     """The ABI's maxima in one region: 64 input targets x a 2x2 clamped
     window = 256 features, a 1024-wide hidden layer, 16 output targets
-    (general kernel); the same map's 256-feature record (64-bit collect)."""
+    (layer by layer); the same map's 256-feature record (64-bit collect)."""
     import torch
     g = np.random.default_rng(1024)
     shape = (23, 31)
@@ -437,7 +437,7 @@ def test_limits_max_features_targets_width(compute):
                     [wl.sentinel_like(shape) for _ in range(16)])
     w.model = wl.make_model(5, w.dims, compute)
     got, var = run_infer(w)
-    assert var.startswith("mlp_generic"), var
+    assert var.startswith("mlp_layers"), var
     Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
     assert_close(np.stack([a.reshape(-1) for a in got], 1), Y, RTOL[compute], var)
     m = api.Map(spec, to_dev(fields), _abi.TO)
@@ -518,7 +518,7 @@ def test_determinism_and_batch_order():
 @pytest.mark.parametrize("compute", ["f32", "bf16"])
 def test_generic_shapes_rank3_clamp_strided(compute):
     """A rank-3 clamp/periodic map with steps over strided target views, with
-    a hidden layer wider than the MFMA kernels take (the general kernel) and
+    a hidden layer wider than the MFMA kernels take (layer by layer) and
     with uneven narrow hidden layers (an MFMA kernel, zero-padded)."""
     import torch
     g = np.random.default_rng(77)
@@ -529,7 +529,7 @@ def test_generic_shapes_rank3_clamp_strided(compute):
     F = oracle.n_features(spec, views)
     npts = oracle.n_points(spec, views)
     wide = 200 if compute == "f32" else 600
-    for dims, want in (([F, wide, 24, 3], "mlp_generic"), ([F, 40, 24, 3], "mlp_" + compute)):
+    for dims, want in (([F, wide, 24, 3], "mlp_layers"), ([F, 40, 24, 3], "mlp_" + compute)):
         model = wl.make_model(9, dims, compute)
         outs_np = [wl.sentinel_like((npts,)) for _ in range(3)]
         Y = oracle.infer_rows(spec, views, model)
@@ -544,6 +544,97 @@ def test_generic_shapes_rank3_clamp_strided(compute):
         torch.cuda.synchronize()
         got = np.stack([o.cpu().numpy() for o in outs], 1)
         assert_close(got, Y, RTOL[compute], "%s %s" % (var, dims))
+
+
+@pytest.fixture
+def small_chunks(monkeypatch):
+    """Layer-by-layer plans created under this fixture take chunks of 4096
+    points (the smallest), so a test of ~10^4 points crosses chunk borders
+    and ends on a ragged chunk."""
+    monkeypatch.setenv("HPACML_LAYERS_CHUNK_MB", "1")
+
+
+@pytest.mark.parametrize("compute, dims, acts", [
+    ("bf16", [6, 1024, 512, 256, 1], None),
+    ("bf16", [35, 600, 5], None),
+    ("f32", [9, 300, 200, 1], None),
+    ("f32", [36, 256, 256, 256, 256, 4], None),
+    ("f32", [12, 160, 7], [1, 1]),                   # ReLU on the output layer too
+    ("bf16", [10, 700, 300, 3], [0, 1, 0]),          # an identity hidden layer
+])
+def test_layers_path_chunks_and_tail(compute, dims, acts, small_chunks):
+    """Shapes outside the fused kernels run layer by layer (gather, one
+    matmul per layer with bias and activation in its epilogue, scatter):
+    10,001 points in chunks of 4096 and a ragged last chunk, against the
+    oracle on every point."""
+    n = 10001
+    g = np.random.default_rng(sum(dims) + 3 * len(dims))
+    spec = wl.pointwise_spec(n)
+    w = wl.Workload("layers", 0, compute, dims, spec, spec,
+                    [g.uniform(-1, 1, n).astype(np.float32) for _ in range(dims[0])],
+                    [wl.sentinel_like((n,)) for _ in range(dims[-1])])
+    w.model = wl.make_model(70 + len(dims), dims, compute)
+    if acts is not None:
+        w.model["act"] = list(acts)
+    got, var = run_infer(w)
+    assert var == "mlp_layers_" + compute, var
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    worst, norm = assert_close(np.stack(got, 1), Y, RTOL[compute], var)
+    print("%s %s [%s]: worst scaled %.3e normwise %.3e" % (compute, dims, var, worst, norm))
+
+
+def test_layers_path_in_place_across_chunks(small_chunks):
+    """A 3x3-window step written back into its own fields, one field stored
+    transposed (maps outside the 32-bit form), 6,300 cells in two chunks:
+    the snapshot record keeps the second chunk's inputs from the first
+    chunk's outputs."""
+    import torch
+    w = wl.make("stencil2d", (70, 90))
+    fields = to_dev(w.inputs)
+    fields[1] = torch.from_numpy(np.ascontiguousarray(w.inputs[1].T)).cuda().t()
+    mi = api.Map(w.in_spec, fields, _abi.TO)
+    mo = api.Map(w.out_spec, fields, _abi.FROM)
+    m = api.Model(w.model)
+    var = api.variant(m, mi, mo)
+    assert var == "snapshot+mlp_layers_f32", var
+    exp = [a.copy() for a in w.inputs]
+    api.infer(m, mi, mo)
+    oracle.infer(w.in_spec, exp, w.out_spec, exp, w.model)
+    torch.cuda.synchronize()
+    got = np.stack([f.cpu().numpy().reshape(-1) for f in fields], 1)
+    want = np.stack([a.reshape(-1) for a in exp], 1)
+    assert_close(got, want, RTOL["f32"], "in place across chunks via " + var)
+
+
+@pytest.mark.parametrize("compute", ["f32", "bf16"])
+def test_general_kernel_through_noalloc(compute):
+    """hpacml_infer_noalloc keeps the general fused kernel for shapes that
+    hpacml_infer runs layer by layer (no workspace): both against the
+    oracle."""
+    import torch
+    dims = [9, 300, 40, 2] if compute == "f32" else [9, 640, 40, 2]
+    n = 3001
+    g = np.random.default_rng(5)
+    spec = wl.pointwise_spec(n)
+    ins = [g.uniform(-1, 1, n).astype(np.float32) for _ in range(9)]
+    model = wl.make_model(31, dims, compute)
+    Y = oracle.infer_rows(spec, ins, model)
+    m = api.Model(model)
+    for noalloc in (False, True):
+        outs = to_dev([wl.sentinel_like((n,)) for _ in range(2)])
+        mi = api.Map(spec, to_dev(ins), _abi.TO)
+        mo = api.Map(spec, outs, _abi.FROM)
+        if noalloc:
+            st = torch.cuda.current_stream().cuda_stream
+            assert _abi.lib().hpacml_infer_noalloc(m.handle, mi.handle, mo.handle, st) == _abi.OK
+        else:
+            assert api.variant(m, mi, mo) == "mlp_layers_" + compute
+            api.infer(m, mi, mo)
+        torch.cuda.synchronize()
+        got = np.stack([o.cpu().numpy() for o in outs], 1)
+        assert_close(got, Y, RTOL[compute], "noalloc" if noalloc else "infer")
+        mi.close(), mo.close()
+    m.close()
 
 
 # ------------------------------------------------------------------ errors
@@ -710,7 +801,7 @@ def test_inplace_window_update_general_maps():
     mo = api.Map(w.out_spec, fields, _abi.FROM)
     m = api.Model(w.model)
     var = api.variant(m, mi, mo)
-    assert var == "snapshot+mlp_generic_f32", var
+    assert var == "snapshot+mlp_layers_f32", var
     exp = [a.copy() for a in w.inputs]
     api.infer(m, mi, mo)
     oracle.infer(w.in_spec, exp, w.out_spec, exp, w.model)
