@@ -246,6 +246,13 @@ typedef struct {
 hpacml_status hpacml_cnn_validate(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
                                   const hpacml_layer *layers, int32_t *out_shape);
 
+/* Number of weights and biases hpacml_cnn_create reads from W[l] and b[l]
+ * for each layer of a convolutional model (w_counts[l], b_counts[l], both
+ * [n_layers] arrays the caller owns; 0 and 0 for MAXPOOL2D).  Errors as
+ * hpacml_cnn_validate; NULL count arrays: HPACML_E_INVAL.  No device work. */
+hpacml_status hpacml_cnn_param_counts(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                                      const hpacml_layer *layers, int64_t *w_counts, int64_t *b_counts);
+
 /* Creates a convolutional model for images of height x width x in_channels.
  *   layers: [n_layers], read during the call only.
  *   W[l], b[l]: HOST fp32 (CONV2D [out][in][kh][kw] and [out]; LINEAR

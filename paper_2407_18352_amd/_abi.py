@@ -68,6 +68,8 @@ SIGNATURES = {
                                       C.c_void_p]),
     "hpacml_infer_variant": (C.c_char_p, [C.c_void_p, C.c_void_p, C.c_void_p]),
     "hpacml_cnn_validate": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(C.c_int32)]),
+    "hpacml_cnn_param_counts": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(C.c_int64),
+                                          _P(C.c_int64)]),
     "hpacml_cnn_create": (C.c_int, [C.c_int32, C.c_int32, C.c_int32, C.c_int32, _P(Layer), _P(_P(C.c_float)),
                                     _P(_P(C.c_float)), C.c_int32, _P(C.c_void_p)]),
     "hpacml_region_create": (C.c_int, [C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32, C.c_int64,

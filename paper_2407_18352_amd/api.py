@@ -204,27 +204,17 @@ class CnnModel:
                   for ly in Ls]
         self.b = [None if ly["kind"] == "pool" else np.ascontiguousarray(np.asarray(ly["b"], np.float32))
                   for ly in Ls]
-        # weight and bias sizes per layer, for a description the library
-        # accepts (its own status reports the others)
-        if validate_cnn(spec)[0] == _abi.OK:
-            h, w, c = int(spec["image"][0]), int(spec["image"][1]), int(spec["in_channels"])
-            for l, ly in enumerate(Ls):
-                if ly["kind"] == "pool":
-                    (kh, kw), (sh, sw) = ly["kernel"], ly.get("stride", ly["kernel"])
-                    h, w = (h - kh) // sh + 1, (w - kw) // sw + 1
-                    continue
-                if ly["kind"] == "conv":
-                    (kh, kw), (sh, sw) = ly["kernel"], ly.get("stride", (1, 1))
-                    nw = ly["out"] * c * kh * kw
-                    if ly.get("padding", "valid") == "valid":
-                        h, w = (h - kh) // sh + 1, (w - kw) // sw + 1
-                else:
-                    nw = ly["out"] * h * w * c
-                    h = w = 1
-                c = ly["out"]
-                if self.W[l].size != nw or self.b[l].size != c:
+        # weight and bias sizes per layer, as the library reads them (for a
+        # description it rejects, its own status reports the error below)
+        wc, bc = (C.c_int64 * L)(), (C.c_int64 * L)()
+        H, W = spec["image"]
+        if lib().hpacml_cnn_param_counts(int(spec["in_channels"]), int(H), int(W), L, arr, wc, bc) == _abi.OK:
+            for l in range(L):
+                nw = 0 if self.W[l] is None else self.W[l].size
+                nb = 0 if self.b[l] is None else self.b[l].size
+                if nw != wc[l] or nb != bc[l]:
                     raise ValueError("layer %d: weights of %d and biases of %d values, expected %d and %d"
-                                     % (l, self.W[l].size, self.b[l].size, nw, c))
+                                     % (l, nw, nb, wc[l], bc[l]))
         null = C.POINTER(C.c_float)()
         Wp = (C.POINTER(C.c_float) * L)(*[null if w is None else w.ctypes.data_as(C.POINTER(C.c_float))
                                           for w in self.W])

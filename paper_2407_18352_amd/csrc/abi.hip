@@ -680,6 +680,28 @@ hpacml_status hpacml_cnn_validate(int32_t in_channels, int32_t height, int32_t w
     return s;
 }
 
+hpacml_status hpacml_cnn_param_counts(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
+                                      const hpacml_layer *layers, int64_t *w_counts, int64_t *b_counts) {
+    CnnPlan p;
+    hpacml_status s = validate_cnn(in_channels, height, width, n_layers, layers, &p);
+    if (s != HPACML_OK)
+        return s;
+    if (!w_counts || !b_counts)
+        return HPACML_E_INVAL;
+    for (int l = 0; l < n_layers; ++l) {
+        const hpacml_layer &y = layers[l];
+        const CnnShape &si = p.shape[l], &so = p.shape[l + 1];
+        if (y.kind == HPACML_LAYER_CONV2D)
+            w_counts[l] = (int64_t)so.c * si.c * y.kernel[0] * y.kernel[1];
+        else if (y.kind == HPACML_LAYER_LINEAR)
+            w_counts[l] = (int64_t)so.c * si.h * si.w * si.c;
+        else
+            w_counts[l] = 0;
+        b_counts[l] = y.kind == HPACML_LAYER_MAXPOOL2D ? 0 : so.c;
+    }
+    return HPACML_OK;
+}
+
 hpacml_status hpacml_cnn_create(int32_t in_channels, int32_t height, int32_t width, int32_t n_layers,
                                 const hpacml_layer *layers, const float *const *W, const float *const *b,
                                 int32_t compute, hpacml_model **out) {

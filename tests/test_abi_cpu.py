@@ -6,6 +6,7 @@ import os
 import re
 import subprocess
 
+import numpy as np
 import pytest
 
 from paper_2407_18352_amd import _abi, api
@@ -25,7 +26,7 @@ def header_functions():
 
 def test_library_exports_every_declared_symbol():
     names = header_functions()
-    assert len(names) == 23
+    assert len(names) == 24
     L = C.CDLL(_abi.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -267,3 +268,24 @@ def test_cnn_validate_shapes_and_errors():
     assert api.validate_cnn(dict(base, image=(0, 4)))[0] == _abi.E_INVAL
     # zero output channels
     assert api.validate_cnn(dict(base, layers=[dict(conv, out=0)]))[0] == _abi.E_INVAL
+
+
+def test_cnn_param_counts_match_the_workload_weights():
+    """hpacml_cnn_param_counts gives the weight and bias sizes of every layer
+    of the two workload stacks (the arrays the workloads draw), zero for the
+    pool; an invalid description and NULL arrays are errors."""
+    import ctypes as C
+    L = _abi.lib()
+    for name in ("weather_cnn", "particle_cnn"):
+        spec = wl.cnn_model(name, "full")
+        n = len(spec["layers"])
+        wc, bc = (C.c_int64 * n)(), (C.c_int64 * n)()
+        H, W = spec["image"]
+        arr = api._layers(spec)
+        assert L.hpacml_cnn_param_counts(spec["in_channels"], H, W, n, arr, wc, bc) == _abi.OK
+        for l, ly in enumerate(spec["layers"]):
+            want_w = 0 if ly["kind"] == "pool" else np.asarray(ly["W"]).size
+            want_b = 0 if ly["kind"] == "pool" else np.asarray(ly["b"]).size
+            assert (wc[l], bc[l]) == (want_w, want_b), (name, l)
+        assert L.hpacml_cnn_param_counts(spec["in_channels"], H, W, n, arr, None, bc) == _abi.E_INVAL
+        assert L.hpacml_cnn_param_counts(0, H, W, n, arr, wc, bc) == _abi.E_INVAL
