@@ -44,7 +44,7 @@ extern "C" {
 #define HPACML_MAX_TARGETS 64     /* arrays per map */
 #define HPACML_MAX_FEATURES 256   /* features per point of one map */
 #define HPACML_MAX_LAYERS 8       /* layers per model */
-#define HPACML_MAX_WIDTH 1024     /* width of any layer */
+#define HPACML_MAX_WIDTH 4096     /* width of any layer */
 #define HPACML_MAX_CNN_WIDTH 65536 /* channels of a convolutional layer, inputs of a LINEAR layer */
 
 typedef enum {
@@ -178,12 +178,15 @@ hpacml_status hpacml_model_validate(int32_t n_layers, const int32_t *dims,
  * (hidden widths up to 128 for fp32, up to 512 for bf16, with limits on
  * depth, input features and outputs per kernel; hidden layers narrower than
  * the kernel's width run zero-padded, which changes no result).  Any
- * other model or map runs layer by layer: a gather kernel, one hipBLASLt
- * matmul per layer (bias and activation applied to the fp32 accumulators in
- * its epilogue; the same rounding points), a scatter kernel, over chunks of
- * points.  That path uses a workspace the model owns (allocated on the first
+ * other model or map runs layer by layer over chunks of points: a kernel
+ * that gathers the inputs (and computes the first layer when the input width
+ * is at most 12), one hipBLASLt matmul per further layer (bias and
+ * activation applied to the fp32 accumulators in its epilogue; the same
+ * rounding points), and a kernel that writes the outputs through the `from`
+ * map (and computes the last layer when it has at most 8 outputs).  That
+ * path uses a workspace the model owns (allocated on the first
  * such call, grown as needed, freed with the model): two activation buffers
- * of one chunk (about 256 MB each; the environment variable
+ * of one chunk (about 1 GB each; the environment variable
  * HPACML_LAYERS_CHUNK_MB, read when the model is created, sets another size),
  * the chunk's fp32 outputs and up to 64 MB of library scratch; calls that
  * share such a model must not overlap in time on different streams, and the

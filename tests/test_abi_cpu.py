@@ -219,7 +219,8 @@ def test_offsets_beyond_extent_wrap():
     ([35, 512, 512, 5], [1, 1, 0], _abi.BF16, _abi.OK),
     ([5], [], _abi.F32, _abi.E_INVAL),
     ([5, 0, 1], [1, 0], _abi.F32, _abi.E_INVAL),
-    ([5, 2048, 1], [1, 0], _abi.F32, _abi.E_UNSUPPORTED),
+    ([5, 4096, 1], [1, 0], _abi.F32, _abi.OK),
+    ([5, 8192, 1], [1, 0], _abi.F32, _abi.E_UNSUPPORTED),
     ([300, 64, 1], [1, 0], _abi.F32, _abi.E_UNSUPPORTED),
     ([5] * 10, [1] * 9, _abi.F32, _abi.E_UNSUPPORTED),
     ([5, 64, 1], [1, 2], _abi.F32, _abi.E_INVAL),

@@ -423,7 +423,7 @@ def test_padded_hidden_layers(compute, dims, want):
 @pytest.mark.parametrize("compute", ["f32", "bf16"])
 def test_limits_max_features_targets_width(compute):
     """The ABI's maxima in one region: 64 input targets x a 2x2 clamped
-    window = 256 features, a 1024-wide hidden layer, 16 output targets
+    window = 256 features, a 4096-wide hidden layer, 16 output targets
     (layer by layer); the same map's 256-feature record (64-bit collect)."""
     import torch
     g = np.random.default_rng(1024)
@@ -433,7 +433,7 @@ def test_limits_max_features_targets_width(compute):
             "bnd": [wl.CLAMP, wl.CLAMP]}
     out_spec = {"rank": 2, "slices": [((0, 0), (1, 1))], "sweep": ((0, 0), shape, (1, 1)),
                 "bnd": [wl.NONE, wl.NONE]}
-    w = wl.Workload("limits", 0, compute, [256, 1024, 16], spec, out_spec, fields,
+    w = wl.Workload("limits", 0, compute, [256, 4096, 16], spec, out_spec, fields,
                     [wl.sentinel_like(shape) for _ in range(16)])
     w.model = wl.make_model(5, w.dims, compute)
     got, var = run_infer(w)
@@ -555,18 +555,30 @@ def small_chunks(monkeypatch):
 
 
 @pytest.mark.parametrize("compute, dims, acts", [
-    ("bf16", [6, 1024, 512, 256, 1], None),
-    ("bf16", [35, 600, 5], None),
+    ("bf16", [6, 1024, 512, 256, 1], None),          # gather + first layer, 2 matmuls, last layer + scatter
+    ("bf16", [35, 600, 5], None),                    # gather, matmul, last layer + scatter
     ("f32", [9, 300, 200, 1], None),
     ("f32", [36, 256, 256, 256, 256, 4], None),
-    ("f32", [12, 160, 7], [1, 1]),                   # ReLU on the output layer too
-    ("bf16", [10, 700, 300, 3], [0, 1, 0]),          # an identity hidden layer
+    ("f32", [12, 160, 7], [1, 1]),                   # no matmul; ReLU on the output layer too
+    ("bf16", [10, 700, 300, 3], [0, 1, 0]),          # an identity first layer
+    ("bf16", [6, 600, 2], None),                     # no matmul
+    ("f32", [10, 300, 12], None),                    # 12 outputs: matmul + scatter
+    ("bf16", [40, 700, 16], [1, 1]),                 # gather, 2 matmuls, scatter; ReLU output
+    ("f32", [9, 3], None),                           # one layer: gather, matmul, scatter
+    ("bf16", [20, 5], None),
+    ("f32", [11, 1000, 1], None),                    # odd input width; 1000 neurons = 250 groups of 4
+    ("bf16", [3, 1000, 9], None),                    # 125 groups of 8; 9 outputs
+    ("bf16", [6, 4096, 1], None),                    # 4096 neurons: gather, 2 matmuls, scatter
+    ("bf16", [6, 2048, 2], None),                    # 256 groups of 8: the widest fused first layer
+    ("f32", [4, 1024, 1500, 1], None),               # 256 groups of 4; 1500 inputs to the last layer
+    ("f32", [9, 2048, 512, 3], None),
 ])
 def test_layers_path_chunks_and_tail(compute, dims, acts, small_chunks):
-    """Shapes outside the fused kernels run layer by layer (gather, one
-    matmul per layer with bias and activation in its epilogue, scatter):
-    10,001 points in chunks of 4096 and a ragged last chunk, against the
-    oracle on every point."""
+    """Shapes outside the fused kernels run layer by layer (first layer fused
+    with the gather for narrow inputs, a matmul per middle layer with bias
+    and activation in its epilogue, last layer fused with the scatter for at
+    most 8 outputs): 10,001 points in chunks of 4096 and a ragged last
+    chunk, against the oracle on every point."""
     n = 10001
     g = np.random.default_rng(sum(dims) + 3 * len(dims))
     spec = wl.pointwise_spec(n)
@@ -606,13 +618,13 @@ def test_layers_path_in_place_across_chunks(small_chunks):
     assert_close(got, want, RTOL["f32"], "in place across chunks via " + var)
 
 
-@pytest.mark.parametrize("compute", ["f32", "bf16"])
-def test_general_kernel_through_noalloc(compute):
+@pytest.mark.parametrize("compute, dims", [("f32", [9, 300, 40, 2]), ("bf16", [9, 640, 40, 2]),
+                                           ("f32", [9, 2500, 40, 2])])
+def test_general_kernel_through_noalloc(compute, dims):
     """hpacml_infer_noalloc keeps the general fused kernel for shapes that
     hpacml_infer runs layer by layer (no workspace): both against the
-    oracle."""
+    oracle, up to a 2500-wide layer (3 points per tile in LDS)."""
     import torch
-    dims = [9, 300, 40, 2] if compute == "f32" else [9, 640, 40, 2]
     n = 3001
     g = np.random.default_rng(5)
     spec = wl.pointwise_spec(n)
