@@ -29,21 +29,23 @@ bool bf16r_supported(int n_layers, const int32_t *dims, const int32_t *act, int 
     return bf16r_gps(H, nh, f_in) <= 2;
 }
 
-// Stream of one tile: the first layer's fragments (m-block j, K-step s at
-// position j * ks1 + s; column F..F+2 = the bias split in three bf16 terms),
-// padded to whole stages, then each hidden layer's (m-block j, K-step s at
-// j * H/16 + s, columns permuted to the B-fragment order).  A fragment is
-// lane l = (i = l % 32, g = l / 32) x 8 elements: A[i][8 g + e].
+// Stream of one tile: the fused region -- the first layer's fragments
+// (column F..F+2 = the bias split in three bf16 terms) interleaved with the
+// first hidden layer's m-block 0 (and 1), at fused_pos_l1 / fused_pos_h0 --
+// padded to whole stages, then the hidden layers' other m-blocks in order
+// (m-block j, K-step s, columns permuted to the B-fragment order).  A
+// fragment is lane l = (i = l % 32, g = l / 32) x 8 elements: A[i][8 g + e].
 void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const float *const *b,
                 std::vector<uint8_t> &buf, size_t *off_w3, size_t *off_bias, BF16RPacked *pk) {
     const int H = dims[1], F = dims[0], Fo = dims[n_layers];
     const int NMB = H / 32, KS = H / 16, nh = n_layers - 2;
     const int ks1 = bf16r_ks1(F);
     const int st = ring_stages(H, nh, ks1);
-    const int fus = (NMB * ks1 + KS + kSF - 1) / kSF;
+    const int fmb = fused_mb(ks1, nh);
+    const int fus = (NMB * ks1 + fmb * KS + kSF - 1) / kSF;
     // stream position of K-step s of m-block j of hidden layer h
     auto pos_hidden = [&](int h, int j, int s) {
-        return h == 0 && j == 0 ? fused_pos_h0(ks1, NMB, s) : fus * kSF - KS + (h * NMB + j) * KS + s;
+        return h == 0 && j < fmb ? fused_pos_h0(ks1, nh, NMB, s, j) : fus * kSF - fmb * KS + (h * NMB + j) * KS + s;
     };
     std::vector<uint16_t> stream((size_t)st * kSF * 64 * 8, 0);
     auto put = [&](int pos, int l, int e, uint16_t v) { stream[((size_t)pos * 64 + l) * 8 + e] = v; };
@@ -60,7 +62,7 @@ void bf16r_pack(int n_layers, const int32_t *dims, const float *const *W, const 
                         split_bias(b[0][o], t);
                         v = t[k - F];
                     }
-                    put(fused_pos_l1(ks1, j, s), l, e, v);
+                    put(fused_pos_l1(ks1, nh, j, s), l, e, v);
                 }
     for (int h = 0; h < nh; ++h)
         for (int j = 0; j < NMB; ++j)

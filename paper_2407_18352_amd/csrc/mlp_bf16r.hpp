@@ -241,14 +241,26 @@ __device__ __forceinline__ void static_for(Fn &&fn) {
 }
 
 // Tile geometry and the weight stream of one tile.  The stream starts with
-// layer 1 interleaved with m-block 0 of the first hidden layer (the fused
+// layer 1 interleaved with the first hidden layer's m-block 0 (the fused
 // region, padded to whole stages), in the order the kernel consumes them:
 // for each layer-1 m-block j its K-steps, then (j >= 2) K-steps 2j - 4 and
 // 2j - 3 of the hidden m-block 0; its last four K-steps close the region.
+// A first layer of one K-step leaves too few matrix instructions beside its
+// epilogues; when another hidden layer follows (so the first one's outputs
+// go to registers, not to the output layer), hidden m-block 1 joins the
+// region: each of those K-steps is taken for m-block 0 and then m-block 1.
 // The hidden layers' other m-blocks follow, K-step by K-step.
-constexpr int fused_pos_l1(int ks1, int j, int s) { return j * ks1 + s + 2 * (j > 2 ? j - 2 : 0); }
-constexpr int fused_pos_h0(int ks1, int nmb, int k) {
-    return k < 2 * nmb - 4 ? (k / 2 + 3) * ks1 + k : nmb * ks1 + k;
+constexpr bool fuse2(int ks1, int nh) { return ks1 == 1 && nh >= 2; }
+constexpr int fused_mb(int ks1, int nh) { return fuse2(ks1, nh) ? 2 : 1; }
+constexpr int fused_pos_l1(int ks1, int nh, int j, int s) {
+    return fuse2(ks1, nh) ? (j <= 2 ? j : 5 * j - 8) : j * ks1 + s + 2 * (j > 2 ? j - 2 : 0);
+}
+// hidden m-block m (< fused_mb) of the first hidden layer, K-step k
+constexpr int fused_pos_h0(int ks1, int nh, int nmb, int k, int m) {
+    if (!fuse2(ks1, nh))
+        return k < 2 * nmb - 4 ? (k / 2 + 3) * ks1 + k : nmb * ks1 + k;
+    return k < 2 * nmb - 4 ? fused_pos_l1(ks1, nh, k / 2 + 2, 0) + 1 + 2 * (k % 2) + m
+                           : fused_pos_l1(ks1, nh, nmb - 1, 0) + 5 + 2 * (k - (2 * nmb - 4)) + m;
 }
 
 template <int H, int NH, int KS1>
@@ -257,18 +269,21 @@ struct RGeo {
     static constexpr int KS = H / 16;                     // K-steps of a hidden layer
     static constexpr int L1F = NMB * KS1;                 // first-layer fragments
     static constexpr int HF = NMB * KS;                   // fragments of a hidden layer
-    static constexpr int FUSF = L1F + KS;                 // fused region: layer 1 + hidden m-block 0
+    static constexpr bool F2 = fuse2(KS1, NH);            // hidden m-block 1 in the fused region
+    static constexpr int FMB = fused_mb(KS1, NH);         // hidden m-blocks in the fused region
+    static constexpr int FUSF = L1F + FMB * KS;           // fused region: layer 1 + those m-blocks
     static constexpr int FUS = (FUSF + kSF - 1) / kSF;    // ... in whole stages
-    static constexpr int ST = FUS + (NH * HF - KS) / kSF; // stages per tile
-    static constexpr int pos_l1(int j, int s) { return fused_pos_l1(KS1, j, s); }
-    static constexpr int pos_h0(int k) { return fused_pos_h0(KS1, NMB, k); }
-    // m-block j of hidden layer l (l = 0: j >= 1)
-    static constexpr int pos_h(int l, int j) { return FUS * kSF - KS + (l * NMB + j) * KS; }
+    static constexpr int ST = FUS + (NH * HF - FMB * KS) / kSF; // stages per tile
+    static constexpr int pos_l1(int j, int s) { return fused_pos_l1(KS1, NH, j, s); }
+    static constexpr int pos_h0(int k, int m) { return fused_pos_h0(KS1, NH, NMB, k, m); }
+    // m-block j of hidden layer l (l = 0: j >= FMB)
+    static constexpr int pos_h(int l, int j) { return FUS * kSF - FMB * KS + (l * NMB + j) * KS; }
     static_assert(KS % kSF == 0, "hidden m-blocks are whole stages");
     static_assert(KS % kR == 0 && (FUS * kSF) % kR == 0, "fragment registers aligned with the layers");
     static_assert(NMB % 2 == 0 && NMB >= 4, "m-blocks go in pairs; the fused region needs four");
     static_assert(KS > 14, "an m-block's K-steps hold the previous epilogue (1-7) and the output indices (10, 14)");
-    static_assert(pos_h0(KS - 1) == FUSF - 1, "the fused region is consumed in order");
+    static_assert(pos_h0(KS - 1, FMB - 1) == FUSF - 1, "the fused region is consumed in order");
+    static_assert(!F2 || pos_h0(0, 0) == pos_l1(2, 0) + 1, "F2: hidden K-steps follow layer-1 m-block 2");
     static_assert(H != 512 || NH == 1, "512-wide activations fill the accumulation registers: one hidden layer");
 };
 
@@ -483,6 +498,7 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
     u32x4 h[NH > 1 ? 2 : 1][KS][2];  // activations: B fragments [K-step][n-block]
     floatx16 acc[2][2];
     floatx16 hacc[2];                // m-block 0 of the first hidden layer
+    floatx16 hacc1[G::F2 ? 2 : 1];   // ... and m-block 1 (F2)
 
     for (int it = 0; tile_of(it) < n_tiles; ++it) {
         const int tile = tile_of(it);
@@ -548,9 +564,13 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             };
             const floatx16 zero = {};
             const floatx16 b00 = bias_of(0, 0);
+            const floatx16 b01 = G::F2 ? bias_of(0, 1) : zero;
             auto h0 = [&](auto K) {
                 constexpr int k = decltype(K)::value;
-                kstep(std::integral_constant<int, G::pos_h0(k)>{}, 0, h[0][k], hacc[0], hacc[1], k == 0, b00);
+                kstep(std::integral_constant<int, G::pos_h0(k, 0)>{}, 0, h[0][k], hacc[0], hacc[1], k == 0, b00);
+                if constexpr (G::F2)
+                    kstep(std::integral_constant<int, G::pos_h0(k, 1)>{}, 0, h[0][k], hacc1[0],
+                          hacc1[G::F2 ? 1 : 0], k == 0, b01);
             };
             static_for<0, NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
@@ -580,8 +600,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
         }
 
         // ---- hidden layers before the last: m-blocks unrolled (their
-        //      activations land in statically indexed registers); m-block 0
-        //      of layer 0 is done
+        //      activations land in statically indexed registers); the
+        //      m-blocks of layer 0 in the fused region are done (their
+        //      epilogues run in the first m-block here)
         static_for<0, NH - 1>([&](auto L) {
             constexpr int l = decltype(L)::value;
             const u32x4(*hin)[2] = h[l % 2];
@@ -591,7 +612,7 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 constexpr int j = decltype(J)::value, q = decltype(Q)::value;
                 hout[2 * j + q / 2][q % 2] = to_agpr(to_b(c[q % 2], q / 2));
             };
-            static_for<(l == 0 ? 1 : 0), NMB>([&](auto J) {
+            static_for<(l == 0 ? G::FMB : 0), NMB>([&](auto J) {
                 constexpr int j = decltype(J)::value;
                 kloop(std::integral_constant<int, G::pos_h(l, j)>{}, 0, std::integral_constant<int, KS>{}, hin,
                       acc[j & 1][0], acc[j & 1][1], bias_of(l, j), [&](auto S) {
@@ -601,9 +622,14 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                               using Q = std::integral_constant<int, s - 1>;
                               if constexpr (l == 0 && j == 1)
                                   epih(JP{}, Q{}, hacc);
+                              else if constexpr (G::F2 && l == 0 && j == 2)
+                                  epih(JP{}, Q{}, hacc1);
                               else
                                   epih(JP{}, Q{}, acc[(j - 1) & 1]);
                           }
+                          // F2: the fused m-block 0's epilogue after m-block 1's
+                          if constexpr (G::F2 && l == 0 && j == 2 && s >= 5 && s <= 8)
+                              epih(std::integral_constant<int, 0>{}, std::integral_constant<int, s - 5>{}, hacc);
                       });
             });
             static_for<0, 4>([&](auto Q) { epih(std::integral_constant<int, NMB - 1>{}, Q, acc[(NMB - 1) & 1]); });
@@ -712,9 +738,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
 int b_feature(int s, int g, int e) { return 32 * (s / 2) + 16 * (s % 2) + 8 * (e / 4) + 4 * g + e % 4; }
 
 int ring_stages(int H, int n_hidden, int ks1) {
-    const int nmb = H / 32, ks = H / 16;
-    const int fus = (nmb * ks1 + ks + kSF - 1) / kSF;
-    return fus + (n_hidden * nmb * ks - ks) / kSF;
+    const int nmb = H / 32, ks = H / 16, fmb = fused_mb(ks1, n_hidden);
+    const int fus = (nmb * ks1 + fmb * ks + kSF - 1) / kSF;
+    return fus + (n_hidden * nmb * ks - fmb * ks) / kSF;
 }
 
 // first-layer K-steps and gathers per ring stage of a shape
