@@ -669,7 +669,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 lout.fresh();
                 const Pt32 pt = locate_lm(lout, b < out.n_points ? b : out.n_points - 1);
                 lout.fresh();
-                sidx[n] = pt.pe + wrap_fix_lm(lout, pt, o_raw);
+                // a pointwise `from` map (no offsets: the usual case) never
+                // leaves its arrays, so only a windowed one needs the fix-up
+                sidx[n] = pt.pe + (o_raw != 0 ? wrap_fix_lm(lout, pt, o_raw) : 0);
             };
             // m-block j into accumulators cur; the epilogue of m-block j - 1
             // (accumulators prev) at K-steps 1, 3, 5, 7; extra(S) after K-step S
