@@ -495,6 +495,60 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
     for (int p = 0; p < kPd; ++p)
         a[p] = *frag_ptr(p);
 
+    // ---- a tile's inputs (X buffer xbuf) as layer-1 B fragments; features
+    //      F..F+2 carry the first-layer bias.  Rows below 16 (KS1 - 1) - 2
+    //      (the fewest inputs of this K-step count) are inputs for every F;
+    //      the others are read from a clamped row unconditionally and then
+    //      masked without a branch: the input itself below F, 1 for the
+    //      three bias columns, 0 above.  Piece (s, n) = K-step s, n-block n,
+    //      in two parts: its LDS reads (xload), then the masking and packing
+    //      (xfinish), issued apart so that waiting for the reads does not
+    //      wait for the weight reads issued in between.
+    constexpr int FMIN = 16 * (KS1 - 1) - 2;
+    int32_t tb = 8 * g - F;                 // feature - F of element 0 of K-step 0 in this lane
+    asm volatile("" : "+v"(tb));
+    u32x4 xb[KS1][2];
+    auto xload = [&](int xbuf, int s, int n, uint32_t (&v)[8]) {
+        const float *xa = (const float *)(lds + xoff + xbuf * xbuf_bytes + xwave);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int f0 = 16 * s + e;
+            if (16 * s + 8 + e < FMIN) {     // resolved at unrolling
+                v[e] = __builtin_bit_cast(uint32_t, xa[(f0 + 8 * g) * 64 + 32 * n + col]);
+            } else {
+                const int32_t t = tb + f0;     // feature - F
+                const int fc = t < 0 ? f0 + 8 * g : F - 1;
+                v[e] = __builtin_bit_cast(uint32_t, xa[fc * 64 + 32 * n + col]);
+            }
+        }
+    };
+    auto xfinish = [&](int s, int n, uint32_t (&v)[8]) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            if (!(16 * s + 8 + e < FMIN)) {
+                const int32_t t = tb + 16 * s + e;
+                uint32_t x = v[e];
+                asm volatile("" : "+v"(x));
+                const uint32_t real = (uint32_t)(t >> 31);               // t < 0
+                const uint32_t one = (uint32_t)((t - 3) >> 31) & 0x3F800000u;  // t < 3
+                v[e] = (x & real) | (one & ~real);
+            }
+        }
+        xb[s][n] = u32x4{pack2(__builtin_bit_cast(float, v[0]), __builtin_bit_cast(float, v[1])),
+                         pack2(__builtin_bit_cast(float, v[2]), __builtin_bit_cast(float, v[3])),
+                         pack2(__builtin_bit_cast(float, v[4]), __builtin_bit_cast(float, v[5])),
+                         pack2(__builtin_bit_cast(float, v[6]), __builtin_bit_cast(float, v[7]))};
+    };
+    // the first tile's inputs (X buffer 0, landed in the prologue)
+#pragma unroll
+    for (int s = 0; s < KS1; ++s)
+#pragma unroll
+        for (int n = 0; n < 2; ++n) {
+            uint32_t v[8];
+            xload(0, s, n, v);
+            xfinish(s, n, v);
+        }
+
     u32x4 h[NH > 1 ? 2 : 1][KS][2];  // activations: B fragments [K-step][n-block]
     floatx16 acc[2][2];
     floatx16 hacc[2];                // m-block 0 of the first hidden layer
@@ -509,44 +563,8 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
             gx = it & 1;
         }
 
-        // ---- this tile's inputs (X buffer it & 1) as layer-1 B fragments;
-        //      features F..F+2 carry the first-layer bias
-        // Rows below 16 (KS1 - 1) - 2 (the fewest inputs of this K-step
-        // count) are inputs for every F; the others are read from a clamped
-        // row unconditionally and then masked without a branch: the input
-        // itself below F, 1 for the three bias columns, 0 above.
-        u32x4 xb[KS1][2];
-        {
-            constexpr int FMIN = 16 * (KS1 - 1) - 2;
-            const float *xa = (const float *)(lds + xoff + (it & 1) * xbuf_bytes + xwave);
-            int32_t tb = 8 * g - F;                 // feature - F of element 0 of K-step 0 in this lane
-            asm volatile("" : "+v"(tb));
-#pragma unroll
-            for (int s = 0; s < KS1; ++s)
-#pragma unroll
-                for (int n = 0; n < 2; ++n) {
-                    uint32_t v[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const int f0 = 16 * s + e;
-                        if (16 * s + 8 + e < FMIN) {     // resolved at unrolling
-                            v[e] = __builtin_bit_cast(uint32_t, xa[(f0 + 8 * g) * 64 + 32 * n + col]);
-                        } else {
-                            const int32_t t = tb + f0;     // feature - F
-                            const int fc = t < 0 ? f0 + 8 * g : F - 1;
-                            uint32_t x = __builtin_bit_cast(uint32_t, xa[fc * 64 + 32 * n + col]);
-                            asm volatile("" : "+v"(x));
-                            const uint32_t real = (uint32_t)(t >> 31);               // t < 0
-                            const uint32_t one = (uint32_t)((t - 3) >> 31) & 0x3F800000u;  // t < 3
-                            v[e] = (x & real) | (one & ~real);
-                        }
-                    }
-                    xb[s][n] = u32x4{pack2(__builtin_bit_cast(float, v[0]), __builtin_bit_cast(float, v[1])),
-                                     pack2(__builtin_bit_cast(float, v[2]), __builtin_bit_cast(float, v[3])),
-                                     pack2(__builtin_bit_cast(float, v[4]), __builtin_bit_cast(float, v[5])),
-                                     pack2(__builtin_bit_cast(float, v[6]), __builtin_bit_cast(float, v[7]))};
-                }
-        }
+        // ---- this tile's inputs are in xb (packed during the previous
+        //      tile's last m-block, or by the prologue for the first tile)
 
         // ---- layer 1, fused with m-block 0 of the first hidden layer: for
         //      each m-block j of layer 1, its K-steps, then the epilogue of
@@ -698,10 +716,26 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 mblock(0, acc[0], acc[1], true, none);
                 mblock(1, acc[1], acc[0], false, indices);
             }
-            for (int j = 2; j < NMB; j += 2) {
+            for (int j = 2; j < NMB - 2; j += 2) {
                 mblock(j, acc[0], acc[1], false, none);
                 mblock(j + 1, acc[1], acc[0], false, none);
             }
+            // the last m-block also packs the next tile's inputs (X buffer
+            // (it + 1) & 1, gathered during the tile before this one): piece
+            // p read after K-step 8 + p, finished after K-step 10 + p, in K-
+            // steps that carry no other vector work
+            uint32_t xv[2][8];
+            const int nbuf = (it + 1) & 1;
+            auto next_inputs = [&](auto S) {
+                constexpr int s = decltype(S)::value, NP = 2 * KS1;
+                if constexpr (s >= 10 && s < 10 + NP)
+                    xfinish((s - 10) / 2, (s - 10) % 2, xv[(s - 10) % 2]);
+                if constexpr (s >= 8 && s < 8 + NP)
+                    xload(nbuf, (s - 8) / 2, (s - 8) % 2, xv[(s - 8) % 2]);
+            };
+            static_assert(KS >= 10 + 2 * KS1, "the next tile's inputs fit in the last m-block");
+            mblock(NMB - 2, acc[0], acc[1], false, none);
+            mblock(NMB - 1, acc[1], acc[0], false, next_inputs);
             static_for<0, 4>([&](auto Q) { epi_part(Q, NMB - 1, acc[1]); });
 
             // ---- scatter: y rows are outputs (row 4 g + r in register r < 4),
