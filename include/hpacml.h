@@ -189,8 +189,9 @@ hpacml_status hpacml_model_validate(int32_t n_layers, const int32_t *dims,
  * of one chunk (about 1 GB each; the environment variable
  * HPACML_LAYERS_CHUNK_MB, read when the model is created, sets another size),
  * the chunk's fp32 outputs and up to 64 MB of library scratch; calls that
- * share such a model must not overlap in time on different streams, and the
- * first call must not be made under stream capture.  Where the library has
+ * share such a model must not overlap in time on different streams.  The
+ * path is not meant for stream capture into a HIP graph (its first call
+ * allocates, and the matmul library may clear its scratch with memsets).  Where the library has
  * no algorithm for a layer, a general fused VALU kernel runs instead. */
 hpacml_status hpacml_model_create(int32_t n_layers, const int32_t *dims,
                                   const float *const *W, const float *const *b,

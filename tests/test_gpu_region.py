@@ -63,6 +63,32 @@ def test_infer_mode_is_hpacml_infer():
     assert r.samples == 0
 
 
+def test_predicated_region_with_a_layer_by_layer_model():
+    """A bond model wider than the fused kernels (9-600-300-1 fp32: the
+    layer-by-layer path) under predicated control: the inferring run equals
+    hpacml_infer bit for bit and the oracle within the fp32 bar; the
+    collecting run records the inputs bit for bit."""
+    import torch
+    s = Setup()
+    s.w.model = wl.make_model(s.w.cfg, [9, 600, 300, 1], "f32")
+    s.model = api.Model(s.w.model)
+    assert api.variant(s.model, s.mi, s.mo) == "mlp_layers_f32"
+    r = api.Region(s.model, s.mi, s.mo, _abi.MODE_PREDICATED, capacity=1)
+    r.run(s.accurate(0), cond=True)
+    torch.cuda.synchronize()
+    got = s.outs[0].cpu().numpy().copy()
+    s.outs[0].fill_(0)
+    api.infer(s.model, s.mi, s.mo)
+    torch.cuda.synchronize()
+    assert np.array_equal(got.view(np.uint32), s.outs[0].cpu().numpy().view(np.uint32))
+    Y = oracle.infer_rows(s.w.in_spec, s.w.inputs, s.w.model)
+    assert_close(got.reshape(-1, 1), Y, RTOL["f32"], "region over mlp_layers_f32")
+    r.run(s.accurate(3), cond=False)
+    inp, out, _ = r.read()
+    assert np.array_equal(inp[0].view(np.uint32), oracle.collect(s.w.in_spec, s.host_inputs()))
+    assert np.array_equal(out[0].reshape(-1), s.pattern(3))
+
+
 def test_collect_mode_records_inputs_outputs_and_time():
     import torch
     s = Setup()
