@@ -1,10 +1,13 @@
 // General-shape fused region kernel: gather -> MLP -> scatter for any layer
-// widths (up to 1024), fp32 or bf16 semantics, plain VALU arithmetic.
+// widths (up to the library's 4096), fp32 or bf16 semantics, plain VALU
+// arithmetic.
 //
-// It serves shapes the MFMA kernels do not cover.  A block owns a tile of P
-// sweep points; the composed input tensor and each layer's activations live
-// in LDS ([P][pitch], two buffers), so nothing but the mapped arrays and the
-// weights touches global memory.  Per layer, thread (o, p) computes
+// It serves the allocation-free entry point for shapes the MFMA kernels do
+// not take (the layer-by-layer path needs a workspace), and is that path's
+// fallback.  A block owns a tile of P sweep points (fewer for wider layers:
+// two buffers within 128 KB of LDS); the composed input tensor and each
+// layer's activations live in LDS ([P][pitch], two buffers), so nothing but
+// the mapped arrays and the weights touches global memory.  Per layer, thread (o, p) computes
 //   acc = b[o] + sum_i W[o][i] * h[p][i]
 // with points fastest across a wave, so a wave reads one weight row
 // (broadcast) and P activation rows (odd pitch: no bank conflicts).
