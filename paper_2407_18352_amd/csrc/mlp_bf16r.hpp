@@ -245,22 +245,23 @@ __device__ __forceinline__ void static_for(Fn &&fn) {
 // region, padded to whole stages), in the order the kernel consumes them:
 // for each layer-1 m-block j its K-steps, then (j >= 2) K-steps 2j - 4 and
 // 2j - 3 of the hidden m-block 0; its last four K-steps close the region.
-// A first layer of one K-step leaves too few matrix instructions beside its
-// epilogues; when another hidden layer follows (so the first one's outputs
-// go to registers, not to the output layer), hidden m-block 1 joins the
-// region: each of those K-steps is taken for m-block 0 and then m-block 1.
+// The epilogues of layer 1 need more matrix instructions beside them than
+// a first layer of one K-step, or one hidden m-block, provides; so hidden
+// m-block 1 joins the region too (each of those K-steps is taken for m-block
+// 0, then m-block 1) when the first layer has one K-step and another hidden
+// layer follows, and when the first hidden layer is the last (its m-blocks'
+// epilogues then feed the output layer in the m-block after the region).
 // The hidden layers' other m-blocks follow, K-step by K-step.
-constexpr bool fuse2(int ks1, int nh) { return ks1 == 1 && nh >= 2; }
+constexpr bool fuse2(int ks1, int nh) { return (ks1 == 1 && nh >= 2) || nh == 1; }
 constexpr int fused_mb(int ks1, int nh) { return fuse2(ks1, nh) ? 2 : 1; }
 constexpr int fused_pos_l1(int ks1, int nh, int j, int s) {
-    return fuse2(ks1, nh) ? (j <= 2 ? j : 5 * j - 8) : j * ks1 + s + 2 * (j > 2 ? j - 2 : 0);
+    return j * ks1 + s + 2 * fused_mb(ks1, nh) * (j > 2 ? j - 2 : 0);
 }
 // hidden m-block m (< fused_mb) of the first hidden layer, K-step k
 constexpr int fused_pos_h0(int ks1, int nh, int nmb, int k, int m) {
-    if (!fuse2(ks1, nh))
-        return k < 2 * nmb - 4 ? (k / 2 + 3) * ks1 + k : nmb * ks1 + k;
-    return k < 2 * nmb - 4 ? fused_pos_l1(ks1, nh, k / 2 + 2, 0) + 1 + 2 * (k % 2) + m
-                           : fused_pos_l1(ks1, nh, nmb - 1, 0) + 5 + 2 * (k - (2 * nmb - 4)) + m;
+    const int fm = fused_mb(ks1, nh);
+    return k < 2 * nmb - 4 ? fused_pos_l1(ks1, nh, k / 2 + 2, ks1 - 1) + 1 + fm * (k % 2) + m
+                           : fused_pos_l1(ks1, nh, nmb - 1, ks1 - 1) + 1 + 2 * fm + fm * (k - (2 * nmb - 4)) + m;
 }
 
 template <int H, int NH, int KS1>
@@ -283,7 +284,8 @@ struct RGeo {
     static_assert(NMB % 2 == 0 && NMB >= 4, "m-blocks go in pairs; the fused region needs four");
     static_assert(KS > 14, "an m-block's K-steps hold the previous epilogue (1-7) and the output indices (10, 14)");
     static_assert(pos_h0(KS - 1, FMB - 1) == FUSF - 1, "the fused region is consumed in order");
-    static_assert(!F2 || pos_h0(0, 0) == pos_l1(2, 0) + 1, "F2: hidden K-steps follow layer-1 m-block 2");
+    static_assert(pos_h0(0, 0) == pos_l1(2, KS1 - 1) + 1, "hidden K-steps follow layer-1 m-block 2");
+    static_assert(pos_l1(3, 0) == pos_h0(1, FMB - 1) + 1, "layer-1 m-block 3 follows two hidden K-steps");
     static_assert(H != 512 || NH == 1, "512-wide activations fill the accumulation registers: one hidden layer");
 };
 
@@ -710,13 +712,27 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 if constexpr (decltype(S)::value == 14)
                     scatter_index(1);
             };
-            if constexpr (NH == 1) {
+            // the first m-block pair after the fused region
+            constexpr int J0 = NH == 1 && G::F2 ? 4 : 2;
+            if constexpr (NH == 1 && G::F2) {
+                // m-blocks 0 and 1 were computed in the fused region: m-block
+                // 2 takes m-block 1's epilogue (K-steps 1-7) and m-block 0's
+                // (K-steps 9-15), and the output indices
+                auto two = [&](auto S) {
+                    constexpr int s = decltype(S)::value;
+                    if constexpr (s == 9 || s == 11 || s == 13 || s == 15)
+                        epi_part(std::integral_constant<int, (s - 9) / 2>{}, 0, hacc);
+                    indices(S);
+                };
+                mblock(2, acc[0], hacc1, false, two);
+                mblock(3, acc[1], acc[0], false, none);
+            } else if constexpr (NH == 1) {
                 mblock(1, acc[1], hacc, false, indices);
             } else {
                 mblock(0, acc[0], acc[1], true, none);
                 mblock(1, acc[1], acc[0], false, indices);
             }
-            for (int j = 2; j < NMB - 2; j += 2) {
+            for (int j = J0; j < NMB - 2; j += 2) {
                 mblock(j, acc[0], acc[1], false, none);
                 mblock(j + 1, acc[1], acc[0], false, none);
             }
