@@ -187,7 +187,8 @@ hpacml_status hpacml_model_validate(int32_t n_layers, const int32_t *dims,
  * path uses a workspace the model owns (allocated on the first
  * such call, grown as needed, freed with the model): two activation buffers
  * of one chunk (about 1 GB each; the environment variable
- * HPACML_LAYERS_CHUNK_MB, read when the model is created, sets another size),
+ * HPACML_LAYERS_CHUNK_MB, read when the model is created, sets another size
+ * from 1 MB to 64 GB),
  * the chunk's fp32 outputs and up to 64 MB of library scratch; calls that
  * share such a model must not overlap in time on different streams.  The
  * path is not meant for stream capture into a HIP graph (its first call

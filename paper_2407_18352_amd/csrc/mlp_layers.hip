@@ -625,10 +625,12 @@ hipError_t layers_create(int n_layers, const int32_t *dims, const int32_t *act, 
     // points per chunk: one activation buffer of about 1 GB (fewer, larger
     // matmuls; measured faster than chunks that fit the 256 MB last-level
     // cache); the environment variable HPACML_LAYERS_CHUNK_MB sets another size
+    // (1 MB to 64 GB; other values are ignored), which also bounds the gather
+    // and scatter grids (chunk x features < 2^31 x 256 threads)
     size_t target = (size_t)1024 << 20;
     if (const char *s = std::getenv("HPACML_LAYERS_CHUNK_MB")) {
         const long v = std::atol(s);
-        if (v > 0 && v <= (1L << 20))
+        if (v > 0 && v <= (1L << 16))
             target = (size_t)v << 20;
     }
     p->first_fused = first_fused;
