@@ -1,7 +1,8 @@
 // Layer-by-layer MLP inference (Sec. IV-B: the surrogate is a stack of
-// Linear/ReLU layers evaluated on the gathered input tensor) for shapes the
-// fused kernels do not take: widths above 512 (bf16) or 128 (fp32), more
-// hidden layers, non-uniform stacks, and maps outside the 32-bit form.
+// Linear/ReLU layers evaluated on the gathered input tensor) for shapes no
+// fused kernel takes, even with its hidden layers zero-padded: hidden widths
+// above 512 (bf16) or 128 (fp32), more hidden layers, inputs or outputs than
+// a kernel's limits, and maps outside the 32-bit form.
 //
 // A chunk of points goes through the layers in turn; activations live in
 // two buffers as rows of bf16 (bf16 models) or fp32, one row per point.
@@ -12,8 +13,8 @@
 //     point; otherwise a gather kernel writes the input rows and the layer
 //     is a matmul like the others.
 //   - Middle layers: one hipBLASLt matmul each, column-major
-//     D[N x C] = W[N x K] X[K x C], the bias and ReLU applied to the fp32
-//     accumulators in its epilogue.
+//     D[N x C] = W[N x K] X[K x C], the bias and the activation (ReLU or
+//     identity) applied to the fp32 accumulators in its epilogue.
 //   - Last layer: with at most 8 outputs, one kernel computes it (8 lanes
 //     per point over 128-byte row segments, a shuffle reduction) and writes
 //     the outputs through the `from` map; otherwise a matmul into fp32 rows
