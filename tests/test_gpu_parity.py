@@ -314,7 +314,10 @@ def test_infer_fast_paths_are_used():
     ("bf16", 512, 7, 2, "mlp_bf16r_h512"), ("bf16", 512, 20, 3, "mlp_bf16r_h512"),
     ("bf16", 512, 45, 5, "mlp_bf16_h512"), ("bf16", 512, 61, 9, "mlp_bf16_h512"),
     ("bf16", 512, 35, 5, "mlp_bf16r_h512"), ("bf16", 512, 30, 8, "mlp_bf16r_h512"),
-    ("bf16", 512, 42, 1, "mlp_bf16r_h512")])
+    ("bf16", 512, 42, 1, "mlp_bf16r_h512"),
+    # 256 wide, one hidden-to-hidden layer: one and two first-layer K-steps
+    ("bf16", 256, 6, 1, "mlp_bf16r_h256"), ("bf16", 256, 13, 4, "mlp_bf16r_h256"),
+    ("bf16", 256, 17, 2, "mlp_bf16r_h256")])
 def test_fast_kernels_input_widths(compute, H, F_in, F_out, want):
     """Every template variant of the MFMA kernels (input width classes,
     widths of hidden layers, output counts), pointwise maps with a ragged
