@@ -551,9 +551,9 @@ def test_generic_shapes_rank3_clamp_strided(compute):
 
 @pytest.fixture
 def small_chunks(monkeypatch):
-    """Layer-by-layer plans created under this fixture take chunks of 4096
-    points (the smallest), so a test of ~10^4 points crosses chunk borders
-    and ends on a ragged chunk."""
+    """Layer-by-layer plans created under this fixture take chunks of 1 MB of
+    activations (at least 4096 points): at widths of 160 and more, a test of
+    ~10^4 points crosses chunk borders and ends on a ragged chunk."""
     monkeypatch.setenv("HPACML_LAYERS_CHUNK_MB", "1")
 
 
@@ -580,8 +580,8 @@ def test_layers_path_chunks_and_tail(compute, dims, acts, small_chunks):
     """Shapes outside the fused kernels run layer by layer (first layer fused
     with the gather for narrow inputs, a matmul per middle layer with bias
     and activation in its epilogue, last layer fused with the scatter for at
-    most 8 outputs): 10,001 points in chunks of 4096 and a ragged last
-    chunk, against the oracle on every point."""
+    most 8 outputs): 10,001 points, for the wide models in chunks of 4096
+    and a ragged last chunk, against the oracle on every point."""
     n = 10001
     g = np.random.default_rng(sum(dims) + 3 * len(dims))
     spec = wl.pointwise_spec(n)
