@@ -282,7 +282,7 @@ struct RGeo {
     static_assert(KS % kSF == 0, "hidden m-blocks are whole stages");
     static_assert(KS % kR == 0 && (FUS * kSF) % kR == 0, "fragment registers aligned with the layers");
     static_assert(NMB % 2 == 0 && NMB >= 4, "m-blocks go in pairs; the fused region needs four");
-    static_assert(KS > 14, "an m-block's K-steps hold the previous epilogue (1-7) and the output indices (10, 14)");
+    static_assert(KS > 15, "an m-block's K-steps hold the previous epilogues (to K-step 15) and the output indices (10, 14)");
     static_assert(pos_h0(KS - 1, FMB - 1) == FUSF - 1, "the fused region is consumed in order");
     static_assert(pos_h0(0, 0) == pos_l1(2, KS1 - 1) + 1, "hidden K-steps follow layer-1 m-block 2");
     static_assert(pos_l1(3, 0) == pos_h0(1, FMB - 1) + 1, "layer-1 m-block 3 follows two hidden K-steps");
@@ -637,9 +637,13 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 kloop(std::integral_constant<int, G::pos_h(l, j)>{}, 0, std::integral_constant<int, KS>{}, hin,
                       acc[j & 1][0], acc[j & 1][1], bias_of(l, j), [&](auto S) {
                           constexpr int s = decltype(S)::value;
-                          if constexpr (s >= 1 && s <= 4 && j > 0) {
+                          // quarter q of the previous m-block's epilogue after
+                          // K-step 1 + q KS / 4 (spread over the loop, so the
+                          // vector work sits between matrix instructions)
+                          constexpr int D = KS / 4;
+                          if constexpr (j > 0 && s >= 1 && (s - 1) % D == 0 && (s - 1) / D < 4) {
                               using JP = std::integral_constant<int, (j > 0 ? j - 1 : 0)>;
-                              using Q = std::integral_constant<int, s - 1>;
+                              using Q = std::integral_constant<int, (s - 1) / D>;
                               if constexpr (l == 0 && j == 1)
                                   epih(JP{}, Q{}, hacc);
                               else if constexpr (G::F2 && l == 0 && j == 2)
@@ -647,9 +651,11 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                               else
                                   epih(JP{}, Q{}, acc[(j - 1) & 1]);
                           }
-                          // F2: the fused m-block 0's epilogue after m-block 1's
-                          if constexpr (G::F2 && l == 0 && j == 2 && s >= 5 && s <= 8)
-                              epih(std::integral_constant<int, 0>{}, std::integral_constant<int, s - 5>{}, hacc);
+                          // F2: the fused m-block 0's epilogue between m-block 1's quarters
+                          if constexpr (G::F2 && l == 0 && j == 2 && s >= 1 + D / 2 && (s - 1 - D / 2) % D == 0 &&
+                                        (s - 1 - D / 2) / D < 4)
+                              epih(std::integral_constant<int, 0>{}, std::integral_constant<int, (s - 1 - D / 2) / D>{},
+                                   hacc);
                       });
             });
             static_for<0, 4>([&](auto Q) { epih(std::integral_constant<int, NMB - 1>{}, Q, acc[(NMB - 1) & 1]); });
@@ -694,7 +700,9 @@ mlp_bf16r_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout, BF16RPa
                 sidx[n] = pt.pe + (o_raw != 0 ? wrap_fix_lm(lout, pt, o_raw) : 0);
             };
             // m-block j into accumulators cur; the epilogue of m-block j - 1
-            // (accumulators prev) at K-steps 1, 3, 5, 7; extra(S) after K-step S
+            // (accumulators prev) at K-steps 1, 3, 5, 7 (spreading them over the
+            // loop, as the hidden layers before the last do, measured slower
+            // here); extra(S) after K-step S
             auto mblock = [&](int j, floatx16 (&cur)[2], floatx16 (&prev)[2], bool first, auto extra) {
                 kloop(P0{}, j * KS, NKS{}, hin, cur[0], cur[1], bias_of(l, j), [&](auto S) {
                     constexpr int s = decltype(S)::value;
