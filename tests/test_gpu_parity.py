@@ -423,6 +423,50 @@ def test_padded_hidden_layers(compute, dims, want):
     print("%s %s [%s]: worst scaled %.3e normwise %.3e" % (compute, dims, var, worst, norm))
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_model_shapes_dispatch(seed):
+    """Seeded random multilayer perceptrons (1-5 layers, widths 1-1100,
+    identity output layer as in the paper's models, random hidden activations
+    in fp32 and ReLU in bf16, 1-40 inputs, 1-20 outputs) on 2,777 points of a rank-2
+    clamped window map or a pointwise map: whichever kernel the library picks
+    (fused, zero-padded, layer by layer) matches the oracle within the bar of
+    the precision."""
+    g = np.random.default_rng(9100 + seed)
+    compute = "bf16" if g.random() < 0.5 else "f32"
+    L = int(g.integers(1, 6))
+    widths = [int(g.choice([g.integers(1, 65), g.integers(64, 300), g.integers(300, 1101)])) for _ in range(L - 1)]
+    F_out = int(g.integers(1, 21))
+    if g.random() < 0.5:
+        # rank-2 clamped window: 1-4 fields x a (1-3) x (1-3) window
+        ny, nx = 41, 67
+        nf, wy, wx = int(g.integers(1, 5)), int(g.integers(1, 4)), int(g.integers(1, 4))
+        spec = {"rank": 2, "slices": [((-(wy // 2), -(wx // 2)), (wy, wx))], "sweep": ((0, 0), (ny, nx), (1, 1)),
+                "bnd": [wl.CLAMP, wl.CLAMP]}
+        ins = [g.standard_normal((ny, nx)).astype(np.float32) for _ in range(nf)]
+        F_in, n = nf * wy * wx, ny * nx
+    else:
+        n = 2777
+        F_in = int(g.integers(1, 41))
+        spec = wl.pointwise_spec(n)
+        ins = [g.uniform(-1, 1, n).astype(np.float32) for _ in range(F_in)]
+    dims = [F_in] + widths + [F_out]
+    model = wl.make_model(60 + seed, dims, compute)
+    if compute == "f32":
+        # bf16 models keep ReLU hidden layers: in identity stacks a hidden
+        # value at a bf16 rounding tie, which an fp32 sum in any order may
+        # round the other way from the fp64 oracle, can move an output past
+        # the bf16 bar (an fp32-accumulating CPU mirror moves it alike).
+        model["act"] = [int(a) for a in g.integers(0, 2, L - 1)] + [wl.IDENTITY]
+    w = wl.Workload("random", 0, compute, dims, spec, wl.pointwise_spec(n), ins,
+                    [wl.sentinel_like((n,)) for _ in range(F_out)])
+    w.model = model
+    got, var = run_infer(w)
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    worst, norm = assert_close(np.stack([a.reshape(-1) for a in got], 1), Y, RTOL[compute],
+                               "%s %s acts %s via %s" % (compute, dims, model["act"], var))
+    print("%s %s acts %s [%s]: worst scaled %.3e" % (compute, dims, model["act"], var, worst))
+
+
 @pytest.mark.parametrize("compute", ["f32", "bf16"])
 def test_limits_max_features_targets_width(compute):
     """The ABI's maxima in one region: 64 input targets x a 2x2 clamped
