@@ -85,18 +85,32 @@ __device__ __forceinline__ void load_bias(const float *bias, int g, floatx16 *ac
 
 template <int NMB, int KS1MAX, bool PF>
 __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatTable32 tin, FeatTable32 tout,
-                                                      F32Packed pk, int32_t n_tiles) {
+                                                      F32Packed pk, int32_t n_tiles, int32_t xcd_ranges) {
     extern __shared__ float lds[];
     const F32Layout lay{NMB, pk.ks1, pk.n_hidden, pk.f_out};
     const int lane = threadIdx.x & 63;
     const int g = lane >> 5;
     const int col = lane & 31;
     const int waves_per_block = blockDim.x >> 6;
-    // XCD-aware order: blocks of one XCD (hardware id % 8) take adjacent tiles
+    // XCD-aware order (blocks of one XCD, hardware id % 8, share an L2).
+    // Pointwise maps: each round of the grid takes adjacent tiles per XCD.
+    // Windowed maps (xcd_ranges, grid a multiple of 8): each XCD walks one
+    // contiguous eighth of the tiles, so the rows a window shares with the
+    // tiles before it are still in that XCD's L2.
     const int nb = gridDim.x;
-    const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
-    const int wave_id = lb * waves_per_block + (threadIdx.x >> 6);
-    const int n_waves = nb * waves_per_block;
+    int wave_id, n_waves, t_end;
+    if (xcd_ranges) {
+        const int per = (n_tiles + 7) / 8;
+        const int x = blockIdx.x % 8;
+        wave_id = x * per + (blockIdx.x / 8) * waves_per_block + (threadIdx.x >> 6);
+        n_waves = (nb / 8) * waves_per_block;
+        t_end = (x + 1) * per < n_tiles ? (x + 1) * per : n_tiles;
+    } else {
+        const int lb = (nb % 8 == 0) ? (blockIdx.x % 8) * (nb / 8) + blockIdx.x / 8 : blockIdx.x;
+        wave_id = lb * waves_per_block + (threadIdx.x >> 6);
+        n_waves = nb * waves_per_block;
+        t_end = n_tiles;
+    }
     const int F = in.n_features;
 
     // ---- gather: lane (col, g) loads feature 2s+g of its point for K-step
@@ -135,7 +149,7 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatT
     // when it is the wave's only tile
     constexpr bool kEarly = NMB == 2 || KS1MAX <= 8;
     bool gathered = false;
-    if (kEarly && wave_id < n_tiles && (kPrefetch || wave_id + n_waves >= n_tiles)) {
+    if (kEarly && wave_id < t_end && (kPrefetch || wave_id + n_waves >= t_end)) {
         gather(wave_id);
         gathered = true;
     }
@@ -149,10 +163,10 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatT
             dstl[i] = src[i];
     }
     __syncthreads();
-    if (kPrefetch && !gathered && wave_id < n_tiles)
+    if (kPrefetch && !gathered && wave_id < t_end)
         gather(wave_id);
 
-    for (int tile = wave_id; tile < n_tiles; tile += n_waves) {
+    for (int tile = wave_id; tile < t_end; tile += n_waves) {
         const int b = tile * 32 + col;
         if (!kPrefetch && !gathered)
             gather(tile);
@@ -163,7 +177,7 @@ __global__ void __launch_bounds__(512) mlp_f32_kernel(Map32 in, Map32 out, FeatT
         for (int s = 0; s < KS1MAX; ++s)
             x[s] = xn[s];
         if (kPrefetch)
-            gather(tile + n_waves < n_tiles ? tile + n_waves : tile);
+            gather(tile + n_waves < t_end ? tile + n_waves : tile);
 #pragma unroll
         for (int s = 0; s < KS1MAX; ++s)
             x[s] = (valid && 2 * s + g < F) ? x[s] : 0.f;
@@ -253,12 +267,19 @@ hipError_t launch_t(const Map32 &in, const Map32 &out, const FeatTable32 &tin, c
     const int64_t need = (n_tiles + waves - 1) / waves;
     if (grid > need)
         grid = need;
+    // windowed maps: one contiguous range of tiles per XCD (see the kernel)
+    bool window = false;
+    for (int d = 0; d < in.rank; ++d)
+        window = window || in.omin[d] != 0 || in.omax[d] != 0;
+    const int32_t xcd_ranges = window && grid % 8 == 0;
     // prefetch only when waves take more than one tile
-    auto kern = n_tiles > grid * waves ? mlp_f32_kernel<NMB, KS1MAX, true> : mlp_f32_kernel<NMB, KS1MAX, false>;
+    const int64_t per_wave = xcd_ranges ? (n_tiles + 7) / 8 : n_tiles, waves_each = xcd_ranges ? grid / 8 * waves : grid * waves;
+    auto kern = per_wave > waves_each ? mlp_f32_kernel<NMB, KS1MAX, true> : mlp_f32_kernel<NMB, KS1MAX, false>;
     hipError_t e = hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, stream, in, out, tin, tout, pk, n_tiles);
+    hipLaunchKernelGGL(kern, dim3((unsigned)grid), dim3(threads), lds, stream, in, out, tin, tout, pk, n_tiles,
+                       xcd_ranges);
     return hipGetLastError();
 }
 
