@@ -528,6 +528,23 @@ def test_one_hot_chain_bitexact(H, n_hidden, compute):
         assert np.array_equal(got[0].view(np.uint32), x.view(np.uint32)), (pick, var)
 
 
+@pytest.mark.parametrize("shape", [(257, 300), (40, 1636)])
+def test_windowed_f32_tile_ranges_per_xcd(shape):
+    """Windowed fp32 launches of a full grid (256 blocks) split the tiles into
+    one contiguous range per XCD: 2,410 tiles (ranges of 302, several tiles
+    per wave, the last range short) and 2,045 tiles (ranges of 256, one tile
+    per wave, the last range 253) match the oracle at every point."""
+    w = wl.make("stencil2d", shape)
+    got, var = run_infer(w)
+    assert var == "mlp_f32_h128_k40"
+    Y = oracle.infer_rows(w.in_spec, w.inputs, w.model)
+    exp = [o.copy() for o in w.outputs]
+    oracle.scatter(w.out_spec, exp, Y)
+    worst, norm = assert_close(np.stack([a.reshape(-1) for a in got], 1),
+                               np.stack([a.reshape(-1) for a in exp], 1), RTOL["f32"], "%s via %s" % (shape, var))
+    print("stencil2d %s [%s]: worst scaled %.3e" % (shape, var, worst))
+
+
 def test_guard_band_and_subsweep():
     """A strided sub-sweep writes exactly its points; everything else keeps the
     sentinel bits."""
